@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of one GPU's share of the fused GEMM + All-Scatter on MI355X.
+
+A step is one call of ``symtile_gemm_all_scatter`` for rank 0 of the
+eight-rank bf16 workload (A [4096, 8192], B_shard [8192, 3584], gathered
+output [4096, 28672] in an 8-slot heap): persistent MFMA GEMM, scatter of
+every tile into all 8 slots, per-tile counters.  Inputs are synthetic
+(seeded, N(0,1)/sqrt(K)) and resident in HBM before timing.
+
+Printed: one JSON line with the GEMM + All-Scatter throughput (TFLOP/s),
+its roofline fraction against the dense bf16 MFMA peak, the heap tile copy
+(2048 x 2048 fp32 per rank, 8 ranks, ring r -> r+1) in GB/s against the
+HBM peak, and the CPU oracle timed on a bounded sample as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "fused GEMM+scatter TFLOP/s (% MFMA peak); heap tile-copy GB/s (% HBM peak)"
+PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0}     # MI355X dense bf16/fp16
+PEAK_HBM_GBS = 8000.0                                   # MI355X HBM3E
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", f)
+                  for f in ("gemm_all_scatter.hip", "symtile_device.h")]
+COPY_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", f)
+                for f in ("tile_copy.hip", "symtile_device.h")]
+
+
+def sources_sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(name: str, sources) -> float | None:
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary
+    ``profiles/<name>``: lines ``bytes_per_dispatch: X`` and ``source_sha: H``.
+    None when absent or when the kernel source changed since it was taken."""
+    path = os.path.join(PROFILES, name)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line:
+                k, v = line.split(":", 1)
+                fields[k.strip().lstrip("- ").strip("`")] = v.strip().strip("`")
+    if fields.get("source_sha") != sources_sha(sources):
+        return None
+    try:
+        return float(fields["bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
+    ap.add_argument("--variant", default="wg_spec", choices=["bulk_sync", "fused_seq", "wg_spec"])
+    ap.add_argument("--tile", default="256x256")
+    ap.add_argument("--gemm-wgs", type=int, default=0)
+    ap.add_argument("--copy-wgs", type=int, default=0)
+    ap.add_argument("--group-m", type=int, default=0)
+    ap.add_argument("--nontemporal", type=int, default=0)
+    ap.add_argument("--copy-tile", type=int, default=128)
+    ap.add_argument("--copy-iters", type=int, default=20)
+    ap.add_argument("--no-copy", action="store_true", help="skip the heap tile-copy leg")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="target CPU time of the oracle baseline sample")
+    return ap.parse_args(argv)
+
+
+def bench_gas(args, torch, sym, workload):
+    wl = workload.GEMM_WORKLOADS[args.workload]
+    tm, tn = (int(x) for x in args.tile.split("x"))
+    variant = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC}[
+        args.variant]
+    A, B = workload.workload_inputs(wl, seed=0)
+    dA, dB = A.cuda(), B.cuda()
+    tiles = -(-wl.M // tm) * -(-wl.N_local // tn)
+    slot = wl.M * wl.N_gathered * 2 + wl.world * tiles * 4 + (1 << 16)
+    heap = sym.Heap(wl.world, slot)
+    out = sym.GatheredOutput(heap, wl.M, wl.N_local, workload.torch_dtype(wl.dtype), tm, tn)
+    kw = dict(gemm_wgs=args.gemm_wgs, copy_wgs=args.copy_wgs, nontemporal=args.nontemporal,
+              group_m=args.group_m)
+
+    def step():
+        out.run(dA, dB, 0, variant, **kw)
+
+    for _ in range(args.warmup):
+        step()
+    heap.barrier()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record()
+    for i in range(K):
+        ev[i][0].record()
+        step()
+        ev[i][1].record()
+    t_all1.record()
+    torch.cuda.synchronize()
+    heap.barrier()        # raises if a device-side wait timed out
+    total_ms = t_all0.elapsed_time(t_all1)
+    per_launch_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = total_ms / K
+    flops = wl.flops
+    kernel_s = (sum(per_launch_ms) / K) * 1e-3
+    achieved = flops / kernel_s / 1e12
+    peak = PEAK_MFMA_TFLOPS[wl.dtype]
+    traffic = counter_traffic(f"gas_kernel_{wl.name}_pmc.txt", KERNEL_SOURCES)
+    res = {
+        "value": flops / (ms_per_step * 1e-3) / 1e12,
+        "ms_per_step": ms_per_step,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": traffic,
+                     "kernel": "gas_kernel<%d,%d,%s>" % (tm, tn, wl.dtype),
+                     "algorithmic_flops_per_launch": flops,
+                     "avg_launch_ms": kernel_s * 1e3,
+                     "min_launch_ms": min(per_launch_ms)},
+        "config": {"workload": wl.name, "M": wl.M, "K": wl.K, "N_local": wl.N_local,
+                   "world_size": wl.world, "rank": 0, "N_gathered": wl.N_gathered,
+                   "variant": args.variant, "tile": args.tile, "gemm_wgs": args.gemm_wgs,
+                   "copy_wgs": args.copy_wgs, "nontemporal": args.nontemporal},
+        "dtype": wl.dtype,
+    }
+    heap.close()
+    return res, wl, A, B
+
+
+def bench_copy(args, torch, sym, workload):
+    wl = workload.HEAP_COPY
+    nbytes = wl.rows * wl.cols * 4
+    heap = sym.Heap(wl.world, 2 * nbytes + (1 << 20))
+    src, dst = heap.alloc(nbytes), heap.alloc(nbytes)
+    flags = heap.alloc(1 << 16)
+    heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(workload.copy_send(wl).cuda())
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")   # > 256 MB MALL
+    t = args.copy_tile
+    stream = sym.current_stream()
+
+    def launch():
+        sym.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, sym.F32, t, t,
+                              wl.shift, -1, flags, stream)
+
+    for _ in range(3):
+        launch()
+    torch.cuda.synchronize()
+    cold, warm = [], []
+    for i in range(args.copy_iters):
+        flush.zero_()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        launch()
+        b.record()
+        torch.cuda.synchronize()
+        cold.append(a.elapsed_time(b))
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.copy_iters)]
+    for a, b in evs:
+        a.record()
+        launch()
+        b.record()
+    torch.cuda.synchronize()
+    warm = [a.elapsed_time(b) for a, b in evs]
+    heap.barrier()
+    moved = wl.bytes_moved
+    cold_ms = sum(cold) / len(cold)
+    warm_ms = sum(warm) / len(warm)
+    gbs = moved / (cold_ms * 1e-3) / 1e9
+    traffic = counter_traffic(f"tile_copy_kernel_{wl.name}_t{t}_pmc.txt", COPY_SOURCES)
+    heap.close()
+    del flush
+    return {
+        "value": gbs, "unit": "GB/s", "tile": f"{t}x{t}", "workload": wl.name,
+        "bytes_per_launch": moved, "cold_ms": cold_ms, "warm_ms": warm_ms,
+        "warm_GBps": moved / (warm_ms * 1e-3) / 1e9,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": traffic,
+                     "kernel": "tile_copy_kernel", "avg_launch_ms": cold_ms},
+    }
+
+
+def cpu_baseline(args, wl, A, B, workload):
+    """The oracle (GEMM + placement into every slot + counters) timed on the
+    host cores on the first rows of the same workload; TFLOP/s."""
+    import oracle
+    Ab, Bb = workload.bits(A), workload.bits(B)
+    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+
+    def run(rows):
+        st = oracle.GatheredState(wl.world, rows, wl.N_local, 256, 256)
+        t0 = time.perf_counter()
+        oracle.gemm_all_scatter(st, Ab[:rows], Bb, wl.dtype, 0)
+        return time.perf_counter() - t0
+
+    rows = 64
+    dt = run(rows)
+    per_row = dt / rows
+    rows = int(max(64, min(1024, args.cpu_seconds / max(per_row, 1e-9))))
+    dt = run(rows)
+    flops = 2.0 * rows * wl.N_local * wl.K
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"rows 0..{rows - 1} of A (of {wl.M}) for rank 0's shard: fp32 GEMM + "
+                      f"placement into {wl.world} slots + counters, {dt:.2f} s"}
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (the emulated ranks live in one "
+              f"GPU's HBM); --gpus {args.gpus} is not supported", file=sys.stderr)
+        return 2
+    import torch
+
+    import paper_2511_12500_amd as sym
+    import workload
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    res, wl, A, B = bench_gas(args, torch, sym, workload)
+    line = {
+        "metric": METRIC,
+        "value": res["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": res["dtype"],
+        "data": "synthetic",
+        "config": res["config"],
+        "roofline": res["roofline"],
+    }
+    if not args.no_copy:
+        line["tile_copy"] = bench_copy(args, torch, sym, workload)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args, wl, A, B, workload)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,228 @@
+/*
+ * symtile — one GPU's share of the fused GEMM + All-Scatter of
+ * "Iris: First-Class Multi-GPU Programming Experience in Triton"
+ * (arXiv 2511.12500), for AMD Instinct MI355X (gfx950).
+ *
+ * C ABI.  Every entry point returns a symtile_status (0 = success).  All
+ * device work is enqueued on the caller's stream and is asynchronous; no
+ * C++ exception crosses this boundary.  On failure the library keeps a
+ * thread-local message, returned by symtile_last_error().
+ *
+ * Emulation of the symmetric heap on one GPU: the heap is one device
+ * allocation of world_size equally sized slots; slot s plays the heap of
+ * rank s.  Every symmetric allocation has the same offset in every slot, so
+ * "the same object on rank s" is base[s] + offset, exactly the symmetric
+ * layout of Section 3.2 (constructor, steps 3 and 6).
+ */
+#ifndef SYMTILE_H
+#define SYMTILE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct symtile_heap symtile_heap;   /* opaque */
+typedef void* symtile_stream;               /* a hipStream_t; NULL = null stream */
+
+typedef enum {
+    SYMTILE_OK = 0,
+    SYMTILE_EINVAL = -1,        /* bad argument, shape, pointer or rank */
+    SYMTILE_ENOMEM = -2,        /* device allocation or heap exhausted */
+    SYMTILE_EHIP = -3,          /* a HIP runtime call failed */
+    SYMTILE_ETIMEOUT = -4,      /* a bounded device-side wait expired */
+    SYMTILE_EUNSUPPORTED = -5   /* valid request this build does not run */
+} symtile_status;
+
+typedef enum { SYMTILE_F16 = 1, SYMTILE_BF16 = 2, SYMTILE_F32 = 3 } symtile_dtype;
+
+/* The three schedules of Section 4 built here. */
+typedef enum {
+    SYMTILE_BULK_SYNC = 0,   /* Section 4.1.1: GEMM kernel, then scatter kernel, one stream */
+    SYMTILE_FUSED_SEQ = 1,   /* Section 4.2.1: each tile stored to every rank after its K loop */
+    SYMTILE_WG_SPEC = 2      /* Section 4.2.2: producer WGs compute, consumer WGs scatter */
+} symtile_variant;
+
+/* Atomic verbs of the device API (Section 3.3.3, device API table). */
+typedef enum {
+    SYMTILE_ATOMIC_ADD = 0, SYMTILE_ATOMIC_XCHG = 1, SYMTILE_ATOMIC_CAS = 2,
+    SYMTILE_ATOMIC_AND = 3, SYMTILE_ATOMIC_OR = 4, SYMTILE_ATOMIC_XOR = 5,
+    SYMTILE_ATOMIC_MIN = 6, SYMTILE_ATOMIC_MAX = 7
+} symtile_atomic_op;
+typedef enum { SYMTILE_RELAXED = 0, SYMTILE_ACQUIRE = 1, SYMTILE_RELEASE = 2,
+               SYMTILE_ACQ_REL = 3 } symtile_sem;
+typedef enum { SYMTILE_SCOPE_BLOCK = 0, SYMTILE_SCOPE_GPU = 1,
+               SYMTILE_SCOPE_SYS = 2 } symtile_scope;
+
+/* Launch configuration of symtile_gemm_all_scatter.  Zero fields take the
+ * documented defaults. */
+typedef struct {
+    int variant;          /* symtile_variant */
+    int tile_m, tile_n;   /* output tile; (64,64) (128,128) (256,128) (256,256);
+                             0,0 = 256x256 */
+    int gemm_wgs;         /* producer workgroups; 0 = min(tiles, CU count) for
+                             BULK_SYNC/FUSED_SEQ, CU count - copy_wgs for WG_SPEC */
+    int copy_wgs;         /* WG_SPEC consumers (0 = CU count / 8) and BULK_SYNC
+                             scatter-kernel workgroups (0 = CU count) */
+    uint32_t epoch;       /* WG_SPEC: consumers wait until ready[tile] >= epoch,
+                             so ready must hold epoch - 1 on entry and holds
+                             epoch after the call; 0 is taken as 1 */
+    uint32_t spin_limit;  /* polls of one consumer wait before it gives up and
+                             raises SYMTILE_ETIMEOUT; 0 = 1<<22 */
+    int nontemporal;      /* 1: streaming (non-temporal) stores of the output */
+    int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
+} symtile_gas_config;
+
+/* ---- heap (Section 3.2: constructor steps 3 and 6, host API table) -------- */
+
+/* Create a heap of world_size slots of at least slot_bytes each on HIP
+ * device `device`.  The slot stride is slot_bytes rounded up to 2 MiB.  The
+ * library allocates (hipMalloc) and owns the memory, zeroes it, and builds
+ * the device array of per-slot base addresses.  world_size in [1, 8].
+ * Errors: EINVAL (bad device, world_size, slot_bytes == 0), ENOMEM, EHIP. */
+symtile_status symtile_heap_create(int device, int world_size, size_t slot_bytes,
+                                   symtile_heap** out);
+
+/* Same, over caller-owned device memory [base, base + total_bytes) on
+ * `device` (e.g. a framework tensor).  base must be 256-byte aligned and
+ * total_bytes >= world_size * slot stride.  The memory is not zeroed and is
+ * never freed by the library; it must outlive the heap. */
+symtile_status symtile_heap_create_on(int device, int world_size, size_t slot_bytes,
+                                      void* base, size_t total_bytes, symtile_heap** out);
+
+/* Release the heap (and its memory if the library allocated it).  Waits for
+ * the device.  NULL is accepted. */
+symtile_status symtile_heap_destroy(symtile_heap* h);
+
+/* Symmetric bump allocation: reserve `bytes` at the same offset in every
+ * slot, aligned to `align` (a power of two; 0 = 256).  *offset_out receives
+ * the offset from the slot base.  No per-allocation free.  ENOMEM when the
+ * slot is full. */
+symtile_status symtile_heap_alloc(symtile_heap* h, size_t bytes, size_t align,
+                                  size_t* offset_out);
+
+/* Device address of `offset` in slot `rank`. */
+symtile_status symtile_heap_ptr(const symtile_heap* h, int rank, size_t offset, void** out);
+
+/* Heap geometry: world size, slot stride, bytes allocated per slot, device. */
+symtile_status symtile_heap_info(const symtile_heap* h, int* world_size, size_t* slot_stride,
+                                 size_t* used, int* device);
+
+/* Per-rank heap bases (Section 3.2, get_heap_bases).  *dev_bases receives
+ * the device array of world_size uint64 addresses (owned by the heap);
+ * host_bases, if non-NULL, receives a copy (world_size entries). */
+symtile_status symtile_heap_bases(const symtile_heap* h, const uint64_t** dev_bases,
+                                  uint64_t* host_bases);
+
+/* Host twin of the device translation (Section 3.3.1): for p inside slot
+ * from_rank, *out = base[to_rank] + (p - base[from_rank]).  EINVAL when p is
+ * not inside slot from_rank or a rank is out of range. */
+symtile_status symtile_translate(const symtile_heap* h, const void* p, int from_rank,
+                                 int to_rank, void** out);
+
+/* Device translation applied to n addresses: out[i] = translate(in[i],
+ * from_rank, to_rank) computed by a kernel with the same device routine the
+ * hot path uses.  in and out are device arrays of n uint64.  Addresses are
+ * not range-checked on the device (the caller checks with the host twin). */
+symtile_status symtile_translate_device(const symtile_heap* h, const uint64_t* in, int n,
+                                        int from_rank, int to_rank, uint64_t* out,
+                                        symtile_stream s);
+
+/* Host barrier (Section 3.2, barrier): wait for the stream (device when
+ * NULL), then read and clear the heap's device error word.  Returns
+ * ETIMEOUT if a device-side wait expired since the last barrier, EHIP if
+ * the device reported an error. */
+symtile_status symtile_barrier(symtile_heap* h, symtile_stream s);
+
+/* Fill `bytes` at `offset` of slot `rank` (every slot when rank < 0) with
+ * the byte `value`, with a fill kernel on stream s (no memset node, so it
+ * may be captured into a graph). */
+symtile_status symtile_heap_fill(symtile_heap* h, int rank, size_t offset, size_t bytes,
+                                 int value, symtile_stream s);
+
+/* ---- device API exercise (Section 3.3.3) --------------------------------- */
+
+/* n_threads device threads each apply atomic `op` with ordering `sem` and
+ * scope `scope` to the uint32 at `offset` of slot to_rank, reached by
+ * translating the address of `offset` in slot from_rank.  Thread t uses
+ * operand + t (ADD/AND/OR/XOR/MIN/MAX/XCHG) or compares with `compare`
+ * and swaps in operand + t (CAS).  If old_out (device, n_threads uint32) is
+ * non-NULL, thread t writes the value it observed there.  Orderings that
+ * do not apply to a read-modify-write are rejected with EINVAL. */
+symtile_status symtile_atomic_exercise(symtile_heap* h, int op, int sem, int scope,
+                                       size_t offset, int from_rank, int to_rank,
+                                       int n_threads, uint32_t operand, uint32_t compare,
+                                       uint32_t* old_out, symtile_stream s);
+
+/* ---- heap tile copy (Section 3.3.2, pointer-based put) -------------------- */
+
+/* For every source rank r (all ranks when only_rank < 0, else only_rank),
+ * copy the rows x cols matrix at offset src_off of slot r, tile by tile
+ * (tile_r x tile_c, ragged edge tiles included), to offset dst_off of slot
+ * (r + shift) mod world through the translated destination address, then
+ * release-publish (agent scope) one uint32 counter per tile at
+ * flag_off + 4 * tile of the destination slot (tile = tr * tiles_c + tc).
+ * Row stride `ld` elements; element size from dtype (2 or 4 bytes).  All
+ * ranks run in one launch.  Requirements: cols*esize, tile_c*esize and
+ * ld*esize multiples of 16; offsets 16-byte aligned; regions inside the
+ * slot; the source and destination regions must not overlap.  EINVAL
+ * otherwise. */
+symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off, int rows,
+                                 int cols, int ld, int dtype, int tile_r, int tile_c,
+                                 int shift, int only_rank, size_t flag_off, symtile_stream s);
+
+/* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
+
+/* Rank `rank`'s share: C_r = A * B_shard with an fp32 accumulator (Section 4
+ * GEMM main loop), rounded to the input dtype (nearest even), stored into the
+ * rank's column block [rank*N_local, (rank+1)*N_local) of the gathered output
+ * in EVERY slot, own slot included (Section 4.2.1), with one arrival counter
+ * per tile per slot incremented with release semantics at agent scope after
+ * that tile's data is in that slot.
+ *
+ *  A              device [M, K] row-major, row stride lda (>= K) elements;
+ *                 any device memory (need not be in the heap).
+ *  B_shard        device [K, N_local] row-major, row stride ldb (>= N_local).
+ *  C_gathered_local  address inside slot `rank` of the gathered output
+ *                 [M, world_size*N_local] row-major (row stride
+ *                 world_size*N_local); the same offset is written in every
+ *                 slot.
+ *  arrived_local  address inside slot `rank` of the counters
+ *                 uint32 [world_size][tiles_m][tiles_n] (rank-major), tiles
+ *                 of cfg tile size; slot s receives arrived[rank][m][n] += 1.
+ *  ready          WG_SPEC only: device uint32 [tiles_m*tiles_n] of
+ *                 producer->consumer counters (any device memory), each
+ *                 equal to cfg->epoch - 1 on entry; ignored (may be NULL)
+ *                 for the other variants.
+ *  dtype          SYMTILE_F16 or SYMTILE_BF16, for A, B and C.
+ *
+ * Requirements: K, N_local, lda, ldb multiples of 8; A and B 16-byte
+ * aligned; M, N_local, K >= 0 (zero sizes are no-ops except K == 0, which
+ * stores zeros).  WG_SPEC requires gemm_wgs + copy_wgs workgroups to be
+ * co-resident (checked; EUNSUPPORTED otherwise).  A consumer wait that
+ * exceeds cfg->spin_limit polls records ETIMEOUT for the next
+ * symtile_barrier, and that consumer abandons its remaining tiles. */
+symtile_status symtile_gemm_all_scatter(symtile_heap* h, const void* A, const void* B_shard,
+                                        void* C_gathered_local, uint32_t* arrived_local,
+                                        uint32_t* ready, int M, int N_local, int K, int lda,
+                                        int ldb, int dtype, int rank, int world_size,
+                                        const symtile_gas_config* cfg, symtile_stream s);
+
+/* Number of compute units of `device` and the largest WG_SPEC grid
+ * (gemm_wgs + copy_wgs) that is co-resident for the given tile shape. */
+symtile_status symtile_device_info(int device, int tile_m, int tile_n, int* cu_count,
+                                   int* max_coresident_wgs);
+
+/* Thread-local message of the last failure in this thread ("" if none). */
+const char* symtile_last_error(void);
+
+/* Library version string. */
+const char* symtile_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SYMTILE_H */

@@ -1,0 +1,400 @@
+// Symmetric heap, translation, barrier, fill and the atomic exercise kernel.
+//
+// The heap follows the constructor of Section 3.2 for one process on one
+// GPU: step 3 (allocate the heap on the device) and step 6 (a device array
+// of every rank's heap base).  Steps 1, 2, 4 and 5 (process group, device
+// per rank, IPC handle exchange and opening) have nothing to do when every
+// rank's heap is a slot of one allocation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "symtile.h"
+#include "symtile_device.h"
+#include "symtile_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+constexpr size_t kSlotAlign = size_t(2) << 20;   // 2 MiB
+constexpr size_t kControlBytes = 256;            // bases[8] + error word + spare
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = false;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) return;
+        ok = hipSetDevice(dev) == hipSuccess;
+    }
+    ~DeviceGuard() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+__global__ void translate_kernel(const uint64_t* __restrict__ in, int n, int from_rank,
+                                 int to_rank, const uint64_t* __restrict__ bases,
+                                 uint64_t* __restrict__ out) {
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) out[i] = symtile::translate_addr(in[i], from_rank, to_rank, bases);
+}
+
+__global__ void fill16_kernel(symtile::u32x4* __restrict__ p, size_t n16, uint32_t word) {
+    symtile::u32x4 v = {word, word, word, word};
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n16;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void fill1_kernel(uint8_t* __restrict__ p, size_t n, uint8_t value) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x)
+        p[i] = value;
+}
+
+// One atomic verb with compile-time order and scope.
+template <int SEM, int SCOPE>
+__device__ uint32_t apply_atomic(int op, uint32_t* p, uint32_t v, uint32_t cmp) {
+    switch (op) {
+        case SYMTILE_ATOMIC_ADD: return symtile::atomic_add<SEM, SCOPE>(p, v);
+        case SYMTILE_ATOMIC_XCHG: return symtile::atomic_xchg<SEM, SCOPE>(p, v);
+        case SYMTILE_ATOMIC_CAS: return symtile::atomic_cas<SEM, SCOPE>(p, cmp, v);
+        case SYMTILE_ATOMIC_AND: return symtile::atomic_and<SEM, SCOPE>(p, v);
+        case SYMTILE_ATOMIC_OR: return symtile::atomic_or<SEM, SCOPE>(p, v);
+        case SYMTILE_ATOMIC_XOR: return symtile::atomic_xor<SEM, SCOPE>(p, v);
+        case SYMTILE_ATOMIC_MIN: return symtile::atomic_min<SEM, SCOPE>(p, v);
+        default: return symtile::atomic_max<SEM, SCOPE>(p, v);
+    }
+}
+
+template <int SCOPE>
+__device__ uint32_t apply_sem(int op, int sem, uint32_t* p, uint32_t v, uint32_t cmp) {
+    switch (sem) {
+        case SYMTILE_RELAXED: return apply_atomic<__ATOMIC_RELAXED, SCOPE>(op, p, v, cmp);
+        case SYMTILE_ACQUIRE: return apply_atomic<__ATOMIC_ACQUIRE, SCOPE>(op, p, v, cmp);
+        case SYMTILE_RELEASE: return apply_atomic<__ATOMIC_RELEASE, SCOPE>(op, p, v, cmp);
+        default: return apply_atomic<__ATOMIC_ACQ_REL, SCOPE>(op, p, v, cmp);
+    }
+}
+
+__global__ void atomic_exercise_kernel(uint32_t* local_word, int from_rank, int to_rank,
+                                       const uint64_t* __restrict__ bases, int op, int sem,
+                                       int scope, int n, uint32_t operand, uint32_t compare,
+                                       uint32_t* __restrict__ old_out) {
+    int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= n) return;
+    uint32_t* p = symtile::translate(local_word, from_rank, to_rank, bases);
+    uint32_t v = operand + (uint32_t)t;
+    uint32_t old;
+    switch (scope) {
+        case SYMTILE_SCOPE_BLOCK:
+            old = apply_sem<__HIP_MEMORY_SCOPE_WORKGROUP>(op, sem, p, v, compare);
+            break;
+        case SYMTILE_SCOPE_GPU:
+            old = apply_sem<__HIP_MEMORY_SCOPE_AGENT>(op, sem, p, v, compare);
+            break;
+        default:
+            old = apply_sem<__HIP_MEMORY_SCOPE_SYSTEM>(op, sem, p, v, compare);
+            break;
+    }
+    if (old_out) old_out[t] = old;
+}
+
+symtile_status check_heap(const symtile_heap* h) {
+    if (!h) return symtile_host::fail(SYMTILE_EINVAL, "heap is NULL");
+    return SYMTILE_OK;
+}
+
+symtile_status build_heap(int device, int world, size_t slot_bytes, void* base,
+                          size_t total_bytes, bool owns, symtile_heap** out) {
+    if (!out) return symtile_host::fail(SYMTILE_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (world < 1 || world > SYMTILE_MAX_WORLD)
+        return symtile_host::fail(SYMTILE_EINVAL, "world_size must be in [1, 8]");
+    if (slot_bytes == 0) return symtile_host::fail(SYMTILE_EINVAL, "slot_bytes is 0");
+    int ndev = 0;
+    SYMTILE_HIP(hipGetDeviceCount(&ndev));
+    if (device < 0 || device >= ndev)
+        return symtile_host::fail(SYMTILE_EINVAL, "device " + std::to_string(device) +
+                                                      " out of range");
+    DeviceGuard guard(device);
+    if (!guard.ok) return symtile_host::fail(SYMTILE_EHIP, "hipSetDevice failed");
+    if (slot_bytes > (SIZE_MAX - kSlotAlign) / SYMTILE_MAX_WORLD)
+        return symtile_host::fail(SYMTILE_EINVAL, "slot_bytes too large");
+    const size_t stride = (slot_bytes + kSlotAlign - 1) / kSlotAlign * kSlotAlign;
+    const size_t need = stride * (size_t)world;
+
+    uint8_t* mem = static_cast<uint8_t*>(base);
+    if (owns) {
+        hipError_t e = hipMalloc(reinterpret_cast<void**>(&mem), need);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return symtile_host::fail(SYMTILE_ENOMEM, "hipMalloc of " + std::to_string(need) +
+                                                          " bytes failed: " +
+                                                          hipGetErrorString(e));
+        }
+        e = hipMemset(mem, 0, need);
+        if (e != hipSuccess) {
+            (void)hipFree(mem);
+            return symtile_host::hip_fail(e, "hipMemset(heap)");
+        }
+    } else {
+        if (!mem) return symtile_host::fail(SYMTILE_EINVAL, "base is NULL");
+        if (reinterpret_cast<uintptr_t>(mem) % 256)
+            return symtile_host::fail(SYMTILE_EINVAL, "base must be 256-byte aligned");
+        if (total_bytes < need)
+            return symtile_host::fail(SYMTILE_EINVAL,
+                                      "external memory smaller than world * slot stride (" +
+                                          std::to_string(need) + " bytes)");
+    }
+    void* control = nullptr;
+    hipError_t e = hipMalloc(&control, kControlBytes);
+    if (e != hipSuccess) {
+        if (owns) (void)hipFree(mem);
+        (void)hipGetLastError();
+        return symtile_host::fail(SYMTILE_ENOMEM, "hipMalloc(control block) failed");
+    }
+    symtile_heap* h = new symtile_heap();
+    h->device = device;
+    h->world = world;
+    h->slot_stride = stride;
+    h->used = 0;
+    h->owns_memory = owns;
+    h->base = mem;
+    std::memset(h->host_bases, 0, sizeof h->host_bases);
+    for (int r = 0; r < world; ++r)
+        h->host_bases[r] = reinterpret_cast<uint64_t>(mem) + (uint64_t)r * stride;
+    h->control = control;
+    h->dev_bases = static_cast<uint64_t*>(control);
+    h->dev_err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(control) + 64);
+    unsigned char host_control[kControlBytes];
+    std::memset(host_control, 0, sizeof host_control);
+    std::memcpy(host_control, h->host_bases, sizeof h->host_bases);
+    e = hipMemcpy(control, host_control, kControlBytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        symtile_heap_destroy(h);
+        return symtile_host::hip_fail(e, "hipMemcpy(control block)");
+    }
+    *out = h;
+    return symtile_host::ok();
+}
+
+}  // namespace
+
+namespace symtile_host {
+
+symtile_status fail(symtile_status st, const std::string& msg) {
+    g_last_error = msg;
+    return st;
+}
+
+symtile_status ok() { return SYMTILE_OK; }
+
+symtile_status hip_fail(hipError_t e, const char* what) {
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return SYMTILE_EHIP;
+}
+
+bool in_slot(const symtile_heap* h, const void* p, size_t bytes, int rank) {
+    if (!h || rank < 0 || rank >= h->world) return false;
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    const uint64_t lo = h->host_bases[rank];
+    const uint64_t hi = lo + h->slot_stride;
+    return a >= lo && a <= hi && bytes <= hi - a;
+}
+
+symtile_status set_device(const symtile_heap* h, int* previous) {
+    if (previous) SYMTILE_HIP(hipGetDevice(previous));
+    SYMTILE_HIP(hipSetDevice(h->device));
+    return SYMTILE_OK;
+}
+
+int cu_count(int device) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
+        return 0;
+    return n;
+}
+
+}  // namespace symtile_host
+
+extern "C" {
+
+const char* symtile_last_error(void) { return g_last_error.c_str(); }
+
+const char* symtile_version(void) { return "symtile 0.1 (gfx950)"; }
+
+symtile_status symtile_heap_create(int device, int world_size, size_t slot_bytes,
+                                   symtile_heap** out) {
+    return build_heap(device, world_size, slot_bytes, nullptr, 0, true, out);
+}
+
+symtile_status symtile_heap_create_on(int device, int world_size, size_t slot_bytes,
+                                      void* base, size_t total_bytes, symtile_heap** out) {
+    return build_heap(device, world_size, slot_bytes, base, total_bytes, false, out);
+}
+
+symtile_status symtile_heap_destroy(symtile_heap* h) {
+    if (!h) return SYMTILE_OK;
+    DeviceGuard guard(h->device);
+    symtile_status st = SYMTILE_OK;
+    if (hipDeviceSynchronize() != hipSuccess) st = symtile_host::fail(SYMTILE_EHIP, "sync failed");
+    if (h->owns_memory && h->base) (void)hipFree(h->base);
+    if (h->control) (void)hipFree(h->control);
+    delete h;
+    return st;
+}
+
+symtile_status symtile_heap_alloc(symtile_heap* h, size_t bytes, size_t align,
+                                  size_t* offset_out) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (!offset_out) return symtile_host::fail(SYMTILE_EINVAL, "offset_out is NULL");
+    if (align == 0) align = 256;
+    if (align & (align - 1)) return symtile_host::fail(SYMTILE_EINVAL, "align not a power of 2");
+    if (align > h->slot_stride) return symtile_host::fail(SYMTILE_EINVAL, "align too large");
+    const size_t off = (h->used + align - 1) & ~(align - 1);
+    if (off > h->slot_stride || bytes > h->slot_stride - off)
+        return symtile_host::fail(SYMTILE_ENOMEM, "symmetric heap slot exhausted: " +
+                                                      std::to_string(bytes) + " bytes requested, " +
+                                                      std::to_string(h->slot_stride - h->used) +
+                                                      " free");
+    h->used = off + bytes;
+    *offset_out = off;
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_heap_ptr(const symtile_heap* h, int rank, size_t offset, void** out) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (!out) return symtile_host::fail(SYMTILE_EINVAL, "out is NULL");
+    if (rank < 0 || rank >= h->world) return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (offset > h->slot_stride) return symtile_host::fail(SYMTILE_EINVAL, "offset beyond slot");
+    *out = reinterpret_cast<void*>(h->host_bases[rank] + offset);
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_heap_info(const symtile_heap* h, int* world_size, size_t* slot_stride,
+                                 size_t* used, int* device) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (world_size) *world_size = h->world;
+    if (slot_stride) *slot_stride = h->slot_stride;
+    if (used) *used = h->used;
+    if (device) *device = h->device;
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_heap_bases(const symtile_heap* h, const uint64_t** dev_bases,
+                                  uint64_t* host_bases) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (dev_bases) *dev_bases = h->dev_bases;
+    if (host_bases) std::memcpy(host_bases, h->host_bases, sizeof(uint64_t) * h->world);
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_translate(const symtile_heap* h, const void* p, int from_rank,
+                                 int to_rank, void** out) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (!out) return symtile_host::fail(SYMTILE_EINVAL, "out is NULL");
+    if (from_rank < 0 || from_rank >= h->world || to_rank < 0 || to_rank >= h->world)
+        return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (!symtile_host::in_slot(h, p, 1, from_rank))
+        return symtile_host::fail(SYMTILE_EINVAL, "pointer is not inside the slot of from_rank");
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    *out = reinterpret_cast<void*>(h->host_bases[to_rank] + (a - h->host_bases[from_rank]));
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_translate_device(const symtile_heap* h, const uint64_t* in, int n,
+                                        int from_rank, int to_rank, uint64_t* out,
+                                        symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (n < 0 || (n > 0 && (!in || !out)))
+        return symtile_host::fail(SYMTILE_EINVAL, "bad array arguments");
+    if (from_rank < 0 || from_rank >= h->world || to_rank < 0 || to_rank >= h->world)
+        return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (n == 0) return SYMTILE_OK;
+    DeviceGuard guard(h->device);
+    hipLaunchKernelGGL(translate_kernel, dim3((n + 255) / 256), dim3(256), 0,
+                       static_cast<hipStream_t>(s), in, n, from_rank, to_rank, h->dev_bases, out);
+    SYMTILE_HIP(hipGetLastError());
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_barrier(symtile_heap* h, symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    DeviceGuard guard(h->device);
+    if (s)
+        SYMTILE_HIP(hipStreamSynchronize(static_cast<hipStream_t>(s)));
+    else
+        SYMTILE_HIP(hipDeviceSynchronize());
+    uint32_t err = 0;
+    SYMTILE_HIP(hipMemcpy(&err, h->dev_err, sizeof err, hipMemcpyDeviceToHost));
+    if (err) {
+        const uint32_t zero = 0;
+        SYMTILE_HIP(hipMemcpy(h->dev_err, &zero, sizeof zero, hipMemcpyHostToDevice));
+        if (err & symtile::ERR_TIMEOUT)
+            return symtile_host::fail(SYMTILE_ETIMEOUT,
+                                      "a device-side wait exceeded its spin limit");
+        return symtile_host::fail(SYMTILE_EHIP, "device error word " + std::to_string(err));
+    }
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_heap_fill(symtile_heap* h, int rank, size_t offset, size_t bytes,
+                                 int value, symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (rank >= h->world) return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (offset > h->slot_stride || bytes > h->slot_stride - offset)
+        return symtile_host::fail(SYMTILE_EINVAL, "fill range beyond the slot");
+    if (bytes == 0) return SYMTILE_OK;
+    DeviceGuard guard(h->device);
+    const uint8_t v = static_cast<uint8_t>(value);
+    const uint32_t word = v * 0x01010101u;
+    const int r0 = rank < 0 ? 0 : rank, r1 = rank < 0 ? h->world : rank + 1;
+    hipStream_t st = static_cast<hipStream_t>(s);
+    for (int r = r0; r < r1; ++r) {
+        uint8_t* p = reinterpret_cast<uint8_t*>(h->host_bases[r] + offset);
+        if (reinterpret_cast<uintptr_t>(p) % 16 == 0 && bytes % 16 == 0) {
+            size_t n16 = bytes / 16;
+            unsigned grid = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
+            hipLaunchKernelGGL(fill16_kernel, dim3(grid), dim3(256), 0, st,
+                               reinterpret_cast<symtile::u32x4*>(p), n16, word);
+        } else {
+            unsigned grid = (unsigned)std::min<size_t>((bytes + 255) / 256, 4096);
+            hipLaunchKernelGGL(fill1_kernel, dim3(grid), dim3(256), 0, st, p, bytes, v);
+        }
+        SYMTILE_HIP(hipGetLastError());
+    }
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_atomic_exercise(symtile_heap* h, int op, int sem, int scope,
+                                       size_t offset, int from_rank, int to_rank,
+                                       int n_threads, uint32_t operand, uint32_t compare,
+                                       uint32_t* old_out, symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (op < SYMTILE_ATOMIC_ADD || op > SYMTILE_ATOMIC_MAX)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown atomic op");
+    if (sem < SYMTILE_RELAXED || sem > SYMTILE_ACQ_REL)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown ordering");
+    if (scope < SYMTILE_SCOPE_BLOCK || scope > SYMTILE_SCOPE_SYS)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown scope");
+    if (from_rank < 0 || from_rank >= h->world || to_rank < 0 || to_rank >= h->world)
+        return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (offset % 4 || offset > h->slot_stride - 4)
+        return symtile_host::fail(SYMTILE_EINVAL, "offset must be a 4-byte aligned slot offset");
+    if (n_threads < 0 || n_threads > (1 << 24))
+        return symtile_host::fail(SYMTILE_EINVAL, "n_threads out of range");
+    if (n_threads == 0) return SYMTILE_OK;
+    DeviceGuard guard(h->device);
+    uint32_t* word = reinterpret_cast<uint32_t*>(h->host_bases[from_rank] + offset);
+    hipLaunchKernelGGL(atomic_exercise_kernel, dim3((n_threads + 255) / 256), dim3(256), 0,
+                       static_cast<hipStream_t>(s), word, from_rank, to_rank, h->dev_bases, op,
+                       sem, scope, n_threads, operand, compare, old_out);
+    SYMTILE_HIP(hipGetLastError());
+    return SYMTILE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,137 @@
+// Device-side primitives of the symmetric heap for gfx950 (header-only).
+//
+// These are the device verbs of Section 3.3 (device API table): pointer
+// translation (3.3.1), value-based load/store and pointer-based tile copies
+// (3.3.2), and atomics with an ordering and a scope (3.3.3).  Every verb
+// takes the device array of per-rank heap bases.
+//
+// Memory-model notes (LLVM AMDGPU memory model for gfx9.4/9.5 family):
+// the L2 is private to each XCD, so publishing data to a workgroup on any
+// other XCD needs agent-scope release (the compiler emits the L2 write-back)
+// and the reader needs agent-scope acquire (L2 invalidate).  Everything
+// here goes through __hip_atomic_* and __builtin_amdgcn_fence; no cache
+// maintenance is written by hand.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace symtile {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---- translation (Section 3.3.1) -----------------------------------------
+// p points into the slot of from_rank; the result is the same offset inside
+// the slot of to_rank: bases[to] + (p - bases[from]), in bytes.
+__device__ __forceinline__ uint64_t translate_addr(uint64_t p, int from_rank, int to_rank,
+                                                   const uint64_t* __restrict__ bases) {
+    return bases[to_rank] + (p - bases[from_rank]);
+}
+
+template <class T>
+__device__ __forceinline__ T* translate(T* p, int from_rank, int to_rank,
+                                        const uint64_t* __restrict__ bases) {
+    return reinterpret_cast<T*>(
+        translate_addr(reinterpret_cast<uint64_t>(p), from_rank, to_rank, bases));
+}
+
+// ---- value-based 16-byte access (Section 3.3.2) ----------------------------
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ void st16(void* p, u32x4 v, bool nontemporal) {
+    if (nontemporal)
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+    else
+        *reinterpret_cast<u32x4*>(p) = v;
+}
+
+// load: read 16 bytes at p's counterpart in the heap of `remote`.
+__device__ __forceinline__ u32x4 load(const void* p, int cur, int remote,
+                                      const uint64_t* __restrict__ bases) {
+    return ld16(translate(p, cur, remote, bases));
+}
+
+// store: write 16 bytes to p's counterpart in the heap of `remote`.
+__device__ __forceinline__ void store(void* p, u32x4 v, int cur, int remote,
+                                      const uint64_t* __restrict__ bases, bool nt) {
+    st16(translate(p, cur, remote, bases), v, nt);
+}
+
+// ---- atomics with ordering and scope (Section 3.3.3) ----------------------
+// SEM is a __ATOMIC_* order, SCOPE a __HIP_MEMORY_SCOPE_* constant.
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_add(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_add(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_xchg(uint32_t* p, uint32_t v) {
+    return __hip_atomic_exchange(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_cas(uint32_t* p, uint32_t expected, uint32_t desired) {
+    // failure order: the strongest of relaxed/acquire not above SEM
+    constexpr int FAIL = (SEM == __ATOMIC_ACQUIRE || SEM == __ATOMIC_ACQ_REL) ? __ATOMIC_ACQUIRE
+                                                                              : __ATOMIC_RELAXED;
+    __hip_atomic_compare_exchange_strong(p, &expected, desired, SEM, FAIL, SCOPE);
+    return expected;   // the value observed
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_and(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_and(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_or(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_or(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_xor(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_xor(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_min(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_min(p, v, SEM, SCOPE);
+}
+template <int SEM, int SCOPE>
+__device__ __forceinline__ uint32_t atomic_max(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_max(p, v, SEM, SCOPE);
+}
+
+// ---- per-tile flags ------------------------------------------------------
+// Workgroup-wide publication: every thread makes its own earlier stores
+// visible at agent scope, the workgroup meets at a barrier, then thread 0
+// issues a release fence and increments each of the n counters.  Must be
+// called by every thread of the workgroup.
+__device__ __forceinline__ void wg_release_begin() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+}
+
+__device__ __forceinline__ void flag_add_release(uint32_t* flag) {
+    // caller is one thread that has passed wg_release_begin()
+    __hip_atomic_fetch_add(flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded wait by one thread until *flag >= target.  Polls with relaxed
+// agent-scope loads and a short sleep between polls; the caller follows a
+// successful wait with an agent-scope acquire fence.  Returns false when
+// spin_limit polls pass without success.
+__device__ __forceinline__ bool flag_wait_geq(const uint32_t* flag, uint32_t target,
+                                              uint32_t spin_limit) {
+    for (uint32_t n = 0; n < spin_limit; ++n) {
+        uint32_t v = __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (v >= target) return true;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+// Device error word codes (OR-ed into the heap's error word).
+enum : uint32_t { ERR_TIMEOUT = 1u };
+
+__device__ __forceinline__ void raise_error(uint32_t* err, uint32_t code) {
+    __hip_atomic_fetch_or(err, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+}  // namespace symtile

@@ -1,0 +1,156 @@
+"""Host-side conveniences over the C ABI: a heap whose memory is a torch
+tensor (so slots are zero-copy torch views, as the host API of Section 3.2
+returns tensors living in the heap), and the symmetric buffers of one
+GEMM + All-Scatter problem.  Argument marshalling only."""
+from __future__ import annotations
+
+import torch
+
+from . import _binding as B
+
+_SLOT_ALIGN = 2 << 20
+
+
+def current_stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+class Heap:
+    """A symmetric heap of ``world`` slots on one GPU.
+
+    Memory is a torch uint8 tensor (torch's allocator; the library never frees
+    it) zeroed at creation; ``view`` returns a tensor aliasing one slot."""
+
+    def __init__(self, world: int, slot_bytes: int, device: int = 0):
+        self.world = world
+        self.device = device
+        self.stride = (slot_bytes + _SLOT_ALIGN - 1) // _SLOT_ALIGN * _SLOT_ALIGN
+        self.mem = torch.zeros(world * self.stride, dtype=torch.uint8, device=f"cuda:{device}")
+        self.handle = B.symtile_heap_create_on(device, world, slot_bytes, self.mem.data_ptr(),
+                                               self.mem.numel())
+        w, stride, _, _ = B.symtile_heap_info(self.handle)
+        assert w == world and stride == self.stride
+
+    def close(self) -> None:
+        if self.handle:
+            B.symtile_heap_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def alloc(self, nbytes: int, align: int = 256) -> int:
+        return B.symtile_heap_alloc(self.handle, nbytes, align)
+
+    def ptr(self, rank: int, offset: int) -> int:
+        return B.symtile_heap_ptr(self.handle, rank, offset)
+
+    def bases(self):
+        return B.symtile_heap_bases(self.handle)
+
+    def view(self, rank: int, offset: int, shape, dtype: torch.dtype) -> torch.Tensor:
+        """Tensor of ``shape``/``dtype`` aliasing ``offset`` of slot ``rank``."""
+        n = 1
+        for d in shape:
+            n *= d
+        esize = torch.empty((), dtype=dtype).element_size()
+        start = rank * self.stride + offset
+        if offset % esize or offset + n * esize > self.stride:
+            raise ValueError("view outside the slot or misaligned")
+        return self.mem[start:start + n * esize].view(dtype).view(*shape)
+
+    def slots_view(self, offset: int, shape, dtype: torch.dtype) -> torch.Tensor:
+        """[world, *shape] strided view of the same object in every slot."""
+        esize = torch.empty((), dtype=dtype).element_size()
+        if self.stride % esize:
+            raise ValueError("slot stride not a multiple of the element size")
+        flat = self.mem.view(dtype)
+        n = 1
+        for d in shape:
+            n *= d
+        base = offset // esize
+        strides = [self.stride // esize]
+        acc = 1
+        tail = []
+        for d in reversed(shape):
+            tail.append(acc)
+            acc *= d
+        strides += list(reversed(tail))
+        return flat.as_strided([self.world, *shape], strides, base)
+
+    def barrier(self, stream: int | None = None) -> None:
+        B.symtile_barrier(self.handle, current_stream() if stream is None else stream)
+
+    def fill(self, rank: int, offset: int, nbytes: int, value: int,
+             stream: int | None = None) -> None:
+        B.symtile_heap_fill(self.handle, rank, offset, nbytes, value,
+                            current_stream() if stream is None else stream)
+
+
+def _tiles(n: int, t: int) -> int:
+    return (n + t - 1) // t
+
+
+class GatheredOutput:
+    """The symmetric objects of one GEMM + All-Scatter problem in ``heap``:
+    the gathered output [M, w*N_local] and the arrival counters
+    [w, tiles_m, tiles_n], plus a (non-symmetric) ready counter array."""
+
+    def __init__(self, heap: Heap, M: int, N_local: int, dtype: torch.dtype,
+                 tile_m: int, tile_n: int):
+        self.heap = heap
+        self.M, self.N_local, self.dtype = M, N_local, dtype
+        self.tile_m, self.tile_n = tile_m, tile_n
+        self.tiles_m, self.tiles_n = _tiles(M, tile_m), _tiles(N_local, tile_n)
+        w = heap.world
+        self.c_bytes = M * w * N_local * 2
+        self.c_off = heap.alloc(max(self.c_bytes, 16), 256)
+        self.flag_count = w * self.tiles_m * self.tiles_n
+        self.flag_off = heap.alloc(max(self.flag_count * 4, 4), 256)
+        self.ready = torch.zeros(max(self.tiles_m * self.tiles_n, 1), dtype=torch.int32,
+                                 device=heap.mem.device)
+        self.ready_epoch = 0     # value of every ready counter after the last WG_SPEC call
+
+    def C(self, rank: int) -> torch.Tensor:
+        return self.heap.view(rank, self.c_off, (self.M, self.heap.world * self.N_local),
+                              self.dtype)
+
+    def C_all(self) -> torch.Tensor:
+        return self.heap.slots_view(self.c_off, (self.M, self.heap.world * self.N_local),
+                                    self.dtype)
+
+    def arrived(self, rank: int) -> torch.Tensor:
+        return self.heap.view(rank, self.flag_off,
+                              (self.heap.world, self.tiles_m, self.tiles_n), torch.int32)
+
+    def arrived_all(self) -> torch.Tensor:
+        return self.heap.slots_view(self.flag_off, (self.heap.world, self.tiles_m, self.tiles_n),
+                                    torch.int32)
+
+    def run(self, A: torch.Tensor, B_shard: torch.Tensor, rank: int, variant: int,
+            gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
+            spin_limit: int = 0, epoch: int | None = None, stream: int | None = None) -> None:
+        """One call of rank ``rank`` (enqueued on the stream, asynchronous).
+        For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
+        more than after the previous WG_SPEC call on these buffers."""
+        if A.dtype != self.dtype or B_shard.dtype != self.dtype:
+            raise TypeError("A and B_shard must have the output dtype")
+        if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):
+            raise ValueError("A and B_shard must be contiguous device tensors")
+        M, K = A.shape
+        K2, N = B_shard.shape
+        if M != self.M or N != self.N_local or K2 != K:
+            raise ValueError("shape mismatch")
+        if variant == B.WG_SPEC:
+            self.ready_epoch = self.ready_epoch + 1 if epoch is None else epoch
+        cfg = B.GasConfig(variant=variant, tile_m=self.tile_m, tile_n=self.tile_n,
+                          gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, epoch=max(self.ready_epoch, 1),
+                          spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m)
+        dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
+        B.symtile_gemm_all_scatter(
+            self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),
+            self.heap.ptr(rank, self.flag_off), self.ready.data_ptr(), M, N, K, K, N, dt, rank,
+            self.heap.world, cfg, current_stream() if stream is None else stream)

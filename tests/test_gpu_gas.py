@@ -1,0 +1,297 @@
+"""GPU parity of symtile_gemm_all_scatter against the oracle (through the C ABI).
+
+Bit-exact: placement (sentinel mask), all-slot equality, arrival counters,
+cross-variant heaps.  Values: max|err| <= tol * max|C| (2e-2 bf16, 5e-3 f16)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload
+from tests.gpu_util import (SENTINEL, Problem, check_block, check_gathered, oracle_block,
+                            require_gpu, sym, u16)
+
+pytestmark = pytest.mark.gpu
+
+BULK, FUSED, WGSPEC = 0, 1, 2
+VARIANTS = [BULK, FUSED, WGSPEC]
+VNAMES = {BULK: "bulk_sync", FUSED: "fused_seq", WGSPEC: "wg_spec"}
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+def _blocks(p):
+    return {r: oracle_block(p.A, p.shards[r], p.dtype) for r in range(p.world)}
+
+
+# ---------------------------------------------------------------- tiny two-rank case
+
+@pytest.mark.parametrize("variant", VARIANTS, ids=VNAMES.get)
+def test_tiny_rank0_then_all_ranks(variant):
+    w = workload.TINY
+    p = Problem(w.world, w.M, w.N_local, w.K, w.dtype, w.tile_m, w.tile_n, dist=w.dist)
+    want = _blocks(p)
+    p.sentinel()
+    p.run(0, variant)
+    p.barrier()
+    check_gathered(p, want)
+    arr = p.out.arrived_all().cpu().numpy()
+    assert arr.shape == (2, 2, 2, 1) and int(arr.sum()) == 4   # 2 tiles x 2 slots, rank 0
+    p.run(1, variant)
+    p.barrier()
+    check_gathered(p, want)
+    assert np.all(p.out.arrived_all().cpu().numpy() == 1)      # 4 counters per slot, all 1
+
+
+# ---------------------------------------------------------------- ragged shapes
+
+RAGGED = [
+    # world, M, N_local, K, tile_m, tile_n, dtype
+    (3, 300, 136, 200, 128, 128, "bf16"),
+    (2, 77, 40, 24, 64, 64, "f16"),
+    (4, 130, 264, 72, 256, 128, "bf16"),
+    (5, 257, 264, 520, 256, 256, "f16"),
+    (8, 64, 8, 8, 64, 64, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", RAGGED, ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s" % c)
+@pytest.mark.parametrize("variant", VARIANTS, ids=VNAMES.get)
+def test_ragged_all_ranks(case, variant):
+    world, M, N, K, tm, tn, dtype = case
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=3)
+    want = _blocks(p)
+    p.sentinel()
+    order = list(range(world))[::-1]
+    for i, r in enumerate(order):
+        p.run(r, variant)
+        if i == 0:
+            p.barrier()
+            check_gathered(p, want)     # one rank only: the rest is still sentinel
+    p.barrier()
+    check_gathered(p, want)
+
+
+# ---------------------------------------------------------------- closed forms
+
+def test_identity_A_gives_B_exactly():
+    n = 256
+    A = torch.eye(n, dtype=torch.bfloat16)
+    shards = [workload.gemm_B_shard(n, 128, r, "bf16", "uniform", 5) for r in range(2)]
+    p = Problem(2, n, 128, n, "bf16", 128, 128, A=A, shards=shards)
+    p.sentinel()
+    for r in range(2):
+        p.run(r, FUSED)
+    p.barrier()
+    G = u16(p.out.C_all())
+    for r in range(2):
+        assert np.array_equal(G[1][:, r * 128:(r + 1) * 128], workload.bits(shards[r]))
+
+
+def test_all_ones_f16_is_exact():
+    ones = torch.ones
+    p = Problem(2, 128, 64, 256, "f16", 64, 64, A=ones(128, 256, dtype=torch.float16),
+                shards=[ones(256, 64, dtype=torch.float16)] * 2)
+    p.sentinel()
+    p.run(0, WGSPEC)
+    p.barrier()
+    blk = u16(p.out.C_all())[:, :, :64]
+    assert np.all(blk == 0x5C00)          # binary16 256.0
+
+
+def test_one_hot_B_selects_columns_of_A():
+    rng = np.random.default_rng(4)
+    A = workload.gemm_A(96, 128, "bf16", "uniform", 9)
+    sel = rng.integers(0, 128, size=64)
+    Bf = torch.zeros(128, 64)
+    Bf[torch.from_numpy(sel), torch.arange(64)] = 1.0
+    Bh = Bf.to(torch.bfloat16)
+    p = Problem(3, 96, 64, 128, "bf16", 64, 64, A=A, shards=[Bh] * 3)
+    p.sentinel()
+    p.run(2, BULK)
+    p.barrier()
+    got = u16(p.out.C_all())[0][:, 128:192]
+    assert np.array_equal(got, workload.bits(A)[:, sel])
+
+
+def test_world1_is_a_plain_gemm():
+    M, N, K = 384, 256, 320
+    p = Problem(1, M, N, K, "f16", 128, 128, seed=8)
+    p.sentinel()
+    p.run(0, FUSED)
+    p.barrier()
+    got = u16(p.out.C(0))
+    check_block(got, oracle_block(p.A, p.shards[0], "f16"), "f16", "w=1 vs oracle")
+    lib_ref = (p.dA.float() @ p.dB[0].float()).cpu().numpy()     # independent library GEMM
+    check_block(got, lib_ref, "f16", "w=1 vs torch.matmul")
+
+
+def test_k_zero_stores_zeros():
+    p = Problem(2, 64, 64, 0, "bf16", 64, 64, A=torch.zeros(64, 0, dtype=torch.bfloat16),
+                shards=[torch.zeros(0, 64, dtype=torch.bfloat16)] * 2)
+    p.sentinel()
+    p.run(1, WGSPEC)
+    p.barrier()
+    G = u16(p.out.C_all())
+    assert np.all(G[:, :, 64:] == 0) and np.all(G[:, :, :64] == SENTINEL)
+    assert np.all(p.out.arrived_all().cpu().numpy()[:, 1] == 1)
+
+
+def test_empty_problem_is_a_noop():
+    pkg = sym()
+    heap = pkg.Heap(2, 1 << 20)
+    out = pkg.GatheredOutput(heap, 0, 64, torch.float16, 64, 64)
+    A = torch.zeros(0, 64, dtype=torch.float16, device="cuda")
+    B = torch.zeros(64, 64, dtype=torch.float16, device="cuda")
+    for v in VARIANTS:
+        out.run(A, B, 0, v)
+    heap.barrier()
+
+
+# ---------------------------------------------------------------- evaluation workloads
+
+@pytest.mark.parametrize("variant", VARIANTS, ids=VNAMES.get)
+def test_small_bf16_w8_rank0(variant):
+    w = workload.SMALL_BF16
+    p = Problem(w.world, w.M, w.N_local, w.K, w.dtype, w.tile_m, w.tile_n, dist=w.dist)
+    want = {0: oracle_block(p.A, p.shards[0], w.dtype)}
+    p.sentinel()
+    p.run(0, variant)
+    p.barrier()
+    check_gathered(p, want)
+
+
+def test_small_bf16_w8_every_rank_in_turn():
+    w = workload.SMALL_BF16
+    p = Problem(w.world, w.M, w.N_local, w.K, w.dtype, w.tile_m, w.tile_n, dist=w.dist, seed=1)
+    want = _blocks(p)
+    p.sentinel()
+    for r in range(w.world):
+        p.run(r, WGSPEC)
+    p.barrier()
+    check_gathered(p, want)
+    # identity: every slot holds A @ [B_0 | ... | B_7] (float64 library matmul)
+    full = p.A.double() @ torch.cat([b.double() for b in p.shards], dim=1)
+    G = torch.from_numpy(u16(p.out.C_all())[3].view(np.int16).copy()).view(torch.bfloat16)
+    err = (G.double() - full).abs().max().item()
+    assert err <= 2e-2 * full.abs().max().item()
+
+
+def _large_case(w, seed=0):
+    return Problem(w.world, w.M, w.N_local, w.K, w.dtype, w.tile_m, w.tile_n, dist=w.dist,
+                   seed=seed)
+
+
+@pytest.mark.parametrize("wl", [workload.LARGE_BF16, workload.WIDE_F16], ids=lambda w: w.name)
+def test_full_size_variants_match_oracle_and_each_other(wl):
+    p = _large_case(wl)
+    want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
+    heaps = {}
+    for v in (FUSED, WGSPEC, BULK):
+        p.sentinel()
+        p.run(0, v)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[0]))
+        heaps[v] = u16(p.out.C(5))[:, :wl.N_local].copy()
+    assert np.array_equal(heaps[FUSED], heaps[WGSPEC])
+    assert np.array_equal(heaps[FUSED], heaps[BULK])
+
+
+def test_large_bf16_wg_spec_split_sweep_bitwise():
+    wl = workload.LARGE_BF16
+    pkg = sym()
+    cus, limit = pkg.symtile_device_info(0, wl.tile_m, wl.tile_n)
+    p = _large_case(wl, seed=2)
+    p.sentinel()
+    p.run(0, FUSED)
+    p.barrier()
+    ref = u16(p.out.C(0))[:, :wl.N_local].copy()
+    check_block(ref, oracle_block(p.A, p.shards[0], wl.dtype), wl.dtype, "fused reference")
+    for copy_wgs in (8, 16, 32, 48, 64):
+        gemm_wgs = min(limit, cus) - copy_wgs
+        p.sentinel()
+        p.run(0, WGSPEC, gemm_wgs=gemm_wgs, copy_wgs=copy_wgs)
+        p.barrier()
+        G = u16(p.out.C_all())
+        for s in range(wl.world):
+            assert np.array_equal(G[s][:, :wl.N_local], ref), (copy_wgs, s)
+            assert np.all(G[s][:, wl.N_local:] == SENTINEL), (copy_wgs, s)
+    arr = p.out.arrived_all().cpu().numpy()
+    assert np.all(arr[:, 0] == int(p.calls[0])) and np.all(arr[:, 1:] == 0)
+
+
+def test_nontemporal_and_group_m_do_not_change_bits():
+    wl = workload.SMALL_BF16
+    p = _large_case(wl, seed=4)
+    outs = []
+    for nt, gm in ((0, 0), (1, 0), (0, 1), (1, 8)):
+        p.sentinel()
+        p.run(0, FUSED, nontemporal=nt, group_m=gm)
+        p.barrier()
+        outs.append(u16(p.out.C_all()).copy())
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+# ---------------------------------------------------------------- epochs and failures
+
+def test_repeated_wg_spec_epochs_see_fresh_data():
+    wl = workload.SMALL_BF16
+    p = _large_case(wl, seed=6)
+    want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
+    for epoch in range(1, 4):
+        p.sentinel()
+        p.run(0, WGSPEC, copy_wgs=24)
+        p.barrier()
+        check_gathered(p, want)                     # counters == epoch, data complete
+        assert p.out.ready.cpu().numpy().min() == epoch
+
+
+def test_consumer_timeout_is_reported_not_hung():
+    """Consumers told to wait for an epoch the producers never reach give up
+    after spin_limit polls; the error surfaces at the barrier."""
+    pkg = sym()
+    p = Problem(2, 128, 128, 64, "f16", 64, 64, seed=7)
+    p.out.ready_epoch = 5                   # next call waits for ready >= 6; producers bring 1
+    p.run(0, WGSPEC, spin_limit=2000)
+    with pytest.raises(pkg.SymtileError) as e:
+        p.heap.barrier()
+    assert e.value.name == "ETIMEOUT"
+    p.heap.barrier()                        # the error word was cleared
+
+
+def test_argument_errors():
+    pkg = sym()
+    p = Problem(2, 128, 64, 64, "bf16", 64, 64)
+    h = p.heap.handle
+    cfg = pkg.GasConfig(variant=FUSED, tile_m=64, tile_n=64)
+    c_other = p.heap.ptr(1, p.out.c_off)            # C in the wrong slot for rank 0
+    args = dict(A=p.dA.data_ptr(), B=p.dB[0].data_ptr())
+
+    def call(C, flags, M=128, N=64, K=64, rank=0, world=2, cfg=cfg, dtype=pkg.BF16):
+        pkg.symtile_gemm_all_scatter(h, args["A"], args["B"], C, flags, p.out.ready.data_ptr(),
+                                     M, N, K, K, N, dtype, rank, world, cfg, 0)
+
+    c0, f0 = p.heap.ptr(0, p.out.c_off), p.heap.ptr(0, p.out.flag_off)
+    for bad in (dict(C=c_other, flags=f0), dict(C=c0, flags=f0, K=60),
+                dict(C=c0, flags=f0, rank=2), dict(C=c0, flags=f0, world=3),
+                dict(C=c0, flags=f0, M=100000)):
+        with pytest.raises(pkg.SymtileError) as e:
+            call(**bad)
+        assert e.value.name == "EINVAL", bad
+    with pytest.raises(pkg.SymtileError) as e:
+        call(c0, f0, cfg=pkg.GasConfig(variant=FUSED, tile_m=32, tile_n=32))
+    assert e.value.name == "EUNSUPPORTED"
+    with pytest.raises(pkg.SymtileError) as e:
+        call(c0, f0, cfg=pkg.GasConfig(variant=WGSPEC, tile_m=64, tile_n=64,
+                                       gemm_wgs=100000, copy_wgs=8))
+    assert e.value.name == "EUNSUPPORTED"
+    with pytest.raises(pkg.SymtileError) as e:
+        call(c0, f0, dtype=pkg.F32)
+    assert e.value.name == "EUNSUPPORTED"
+    p.heap.barrier()

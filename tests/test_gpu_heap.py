@@ -1,0 +1,250 @@
+"""GPU tests of the symmetric heap, translation (device vs host twin), the
+atomic verbs of the device API, and the heap tile copy (bit-exact vs oracle)."""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workload
+from tests.gpu_util import require_gpu, sym
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- heap + translation
+
+def test_library_owned_heap_geometry_and_errors():
+    pkg = sym()
+    h = pkg.symtile_heap_create(0, 8, 3 << 20)          # 3 MiB -> 4 MiB stride
+    try:
+        w, stride, used, dev = pkg.symtile_heap_info(h)
+        assert (w, stride, used, dev) == (8, 4 << 20, 0, 0)
+        dev_bases, host = pkg.symtile_heap_bases(h)
+        assert dev_bases and all(host[r] - host[0] == r * stride for r in range(8))
+        assert host[0] % 256 == 0
+        o1 = pkg.symtile_heap_alloc(h, 100, 0)
+        o2 = pkg.symtile_heap_alloc(h, 10, 4096)
+        assert o1 == 0 and o2 == 4096
+        assert pkg.symtile_heap_ptr(h, 5, o2) == host[5] + 4096
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_heap_alloc(h, stride, 0)
+        assert e.value.name == "ENOMEM"
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_heap_alloc(h, 16, 3)
+        assert e.value.name == "EINVAL"
+        # the device bases array holds the same addresses
+        got = (ctypes.c_uint64 * 8)()
+        t = torch.empty(8, dtype=torch.int64, device="cuda")
+        hip = ctypes.CDLL("libamdhip64.so")
+        hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        assert hip.hipMemcpy(ctypes.addressof(got), ctypes.c_void_p(dev_bases), 64, 2) == 0
+        assert list(got) == host
+        del t
+        pkg.symtile_barrier(h, 0)
+    finally:
+        pkg.symtile_heap_destroy(h)
+    with pytest.raises(pkg.SymtileError):
+        pkg.symtile_heap_create(0, 9, 1 << 20)
+    with pytest.raises(pkg.SymtileError):
+        pkg.symtile_heap_create(0, 2, 0)
+
+
+def test_translation_host_twin_invariants():
+    pkg = sym()
+    heap = pkg.Heap(4, 1 << 21)
+    h = heap.handle
+    _, host = heap.bases()
+    rng = np.random.default_rng(0)
+    for _ in range(50):
+        a, b = rng.integers(0, 4, size=2)
+        off = int(rng.integers(0, heap.stride))
+        p = host[a] + off
+        q = pkg.symtile_translate(h, p, int(a), int(b))
+        assert q - host[b] == off                                  # offset preserved
+        assert pkg.symtile_translate(h, q, int(b), int(a)) == p    # round trip
+        assert pkg.symtile_translate(h, p, int(a), int(a)) == p    # identity
+    for bad_p, a in ((host[1], 0), (host[0] - 1, 0), (host[3] + heap.stride, 3)):
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_translate(h, bad_p, a, 1)
+        assert e.value.name == "EINVAL"
+    with pytest.raises(pkg.SymtileError):
+        pkg.symtile_translate(h, host[0], 0, 4)
+
+
+def test_translation_device_matches_host_twin():
+    pkg = sym()
+    heap = pkg.Heap(8, 1 << 21)
+    _, host = heap.bases()
+    rng = np.random.default_rng(1)
+    n = 1000
+    for a, b in ((0, 7), (3, 1), (5, 5), (7, 0)):
+        offs = rng.integers(0, heap.stride, size=n)
+        ins = torch.tensor([host[a] + int(o) for o in offs], dtype=torch.int64, device="cuda")
+        outs = torch.zeros_like(ins)
+        pkg.symtile_translate_device(heap.handle, ins.data_ptr(), n, a, b, outs.data_ptr(),
+                                     pkg.current_stream())
+        heap.barrier()
+        want = [pkg.symtile_translate(heap.handle, host[a] + int(o), a, b) for o in offs]
+        assert outs.cpu().numpy().astype(np.uint64).tolist() == want
+
+
+def test_fill_and_views_alias_the_slots():
+    pkg = sym()
+    heap = pkg.Heap(3, 1 << 20)
+    off = heap.alloc(4096)
+    heap.fill(-1, off, 4096, 0xAB)
+    heap.fill(1, off + 16, 32, 0x01)
+    heap.fill(2, off + 3, 5, 0x7F)                     # unaligned path
+    torch.cuda.synchronize()
+    v = heap.slots_view(off, (4096,), torch.uint8).cpu().numpy()
+    assert np.all(v[0] == 0xAB)
+    assert np.all(v[1][16:48] == 1) and np.all(v[1][:16] == 0xAB) and np.all(v[1][48:] == 0xAB)
+    assert np.all(v[2][3:8] == 0x7F) and v[2][2] == 0xAB and v[2][8] == 0xAB
+    with pytest.raises(pkg.SymtileError):
+        heap.fill(0, heap.stride - 8, 16, 0)
+
+
+# ---------------------------------------------------------------- atomics (device API)
+
+def _atomic(pkg, heap, op, sem, scope, n, operand, init, compare=0, frm=1, to=5):
+    off = heap.alloc(256)
+    heap.slots_view(off, (64,), torch.int32).zero_()
+    heap.view(to, off, (1,), torch.int32).fill_(init)
+    old = torch.zeros(n, dtype=torch.int32, device="cuda")
+    pkg.symtile_atomic_exercise(heap.handle, pkg.ATOMIC_OPS[op], pkg.SEMS[sem], pkg.SCOPES[scope],
+                                off, frm, to, n, operand, compare, old.data_ptr(),
+                                pkg.current_stream())
+    heap.barrier()
+    words = heap.slots_view(off, (64,), torch.int32).cpu().numpy().view(np.uint32)
+    others = [s for s in range(heap.world) if s != to]
+    assert np.all(words[others] == 0), "atomic touched another slot"
+    assert np.all(words[to][1:] == 0)
+    return int(words[to][0]), old.cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("sem", ["relaxed", "acquire", "release", "acq_rel"])
+@pytest.mark.parametrize("scope", ["block", "gpu", "sys"])
+def test_atomic_add_every_order_and_scope(sem, scope):
+    pkg = sym()
+    heap = pkg.Heap(8, 1 << 21)
+    n = 5000
+    final, old = _atomic(pkg, heap, "add", sem, scope, n, 0, 7)
+    # thread t adds t: final = 7 + n(n-1)/2; the observed olds are all distinct
+    assert final == (7 + n * (n - 1) // 2) % 2 ** 32
+    assert len(np.unique(old)) == n
+
+
+def test_atomic_verbs_results():
+    pkg = sym()
+    heap = pkg.Heap(8, 1 << 21)
+    n = 300
+    final, old = _atomic(pkg, heap, "xchg", "acq_rel", "gpu", n, 1000, 5)
+    vals = set(old.tolist()) | {final}
+    assert vals == set(range(1000, 1000 + n)) | {5}               # a permutation chain
+    final, old = _atomic(pkg, heap, "cas", "acq_rel", "gpu", n, 100, 9, compare=9)
+    assert 100 <= final < 100 + n and int(np.sum(old == 9)) == 1  # exactly one winner
+    final, _ = _atomic(pkg, heap, "and", "relaxed", "gpu", 4, 0xFFFFFFF0, 0xFF)
+    assert final == 0xF0 & 0xFFFFFFF1 & 0xFFFFFFF2 & 0xFFFFFFF3
+    final, _ = _atomic(pkg, heap, "or", "release", "sys", n, 0x100, 0)
+    want = 0
+    for t in range(n):
+        want |= 0x100 + t
+    assert final == want
+    final, _ = _atomic(pkg, heap, "xor", "relaxed", "block", n, 3, 0x55)
+    want = 0x55
+    for t in range(n):
+        want ^= 3 + t
+    assert final == want
+    final, _ = _atomic(pkg, heap, "min", "acquire", "gpu", n, 50, 200)
+    assert final == 50
+    final, _ = _atomic(pkg, heap, "max", "acquire", "gpu", n, 50, 200)
+    assert final == 50 + n - 1
+
+
+# ---------------------------------------------------------------- heap tile copy
+
+def _copy_heap(pkg, world, rows, cols, dtype_t):
+    esize = torch.empty((), dtype=dtype_t).element_size()
+    nbytes = rows * cols * esize
+    heap = pkg.Heap(world, 2 * nbytes + (1 << 20))
+    src = heap.alloc(nbytes)
+    dst = heap.alloc(nbytes)
+    flags = heap.alloc(1 << 16)
+    return heap, src, dst, flags
+
+
+@pytest.mark.parametrize("tile", [64, 128, 256])
+def test_heap_tile_copy_workload_bitexact(tile):
+    """All 8 ranks copy send -> recv of rank (r+1) mod 8, 2048 x 2048 fp32."""
+    pkg = sym()
+    wl = workload.HEAP_COPY
+    heap, src, dst, flags = _copy_heap(pkg, wl.world, wl.rows, wl.cols, torch.float32)
+    send = workload.copy_send(wl, seed=0)
+    heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(send.cuda())
+    heap.slots_view(dst, (wl.rows, wl.cols), torch.int32).fill_(-1)
+    pkg.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, pkg.F32, tile, tile,
+                          wl.shift, -1, flags, pkg.current_stream())
+    heap.barrier()
+    recv = heap.slots_view(dst, (wl.rows, wl.cols), torch.float32).cpu().numpy()
+    ntiles = (wl.rows // tile) * (wl.cols // tile)
+    fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
+    want, want_flags = oracle.tile_copy(send.numpy(), np.full_like(send.numpy(), np.nan),
+                                        tile, tile, wl.shift)
+    assert np.array_equal(recv.view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(fl, want_flags.astype(np.int32))
+
+
+@pytest.mark.parametrize("case", [(5, 100, 72, 32, 24, 3, "bf16"), (3, 33, 20, 16, 8, 1, "f32"),
+                                  (8, 64, 64, 64, 64, 7, "f16")])
+def test_heap_tile_copy_ragged_and_single_rank(case):
+    pkg = sym()
+    world, rows, cols, tr, tc, shift, dt = case
+    tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dt]
+    code = {"bf16": pkg.BF16, "f16": pkg.F16, "f32": pkg.F32}[dt]
+    ival = torch.int16 if dt != "f32" else torch.int32
+    heap, src, dst, flags = _copy_heap(pkg, world, rows, cols, tdt)
+    g = torch.Generator().manual_seed(3)
+    send = torch.randint(-2 ** 15, 2 ** 15, (world, rows, cols), generator=g).to(ival)
+    heap.slots_view(src, (rows, cols), ival).copy_(send.cuda())
+    heap.slots_view(dst, (rows, cols), ival).zero_()
+    ntiles = -(-rows // tr) * -(-cols // tc)
+    for only in (world - 1, -1):
+        heap.slots_view(flags, (ntiles,), torch.int32).zero_()
+        heap.slots_view(dst, (rows, cols), ival).zero_()
+        pkg.symtile_tile_copy(heap.handle, src, dst, rows, cols, cols, code, tr, tc, shift,
+                              only, flags, pkg.current_stream())
+        heap.barrier()
+        recv = heap.slots_view(dst, (rows, cols), ival).cpu().numpy()
+        fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
+        want, wf = oracle.tile_copy(send.numpy(), np.zeros_like(send.numpy()), tr, tc, shift,
+                                    only_rank=only)
+        assert np.array_equal(recv, want), only
+        assert np.array_equal(fl, wf.astype(np.int32)), only
+
+
+def test_heap_tile_copy_rejects_bad_arguments():
+    pkg = sym()
+    heap, src, dst, flags = _copy_heap(pkg, 2, 64, 64, torch.float32)
+    h, s = heap.handle, pkg.current_stream()
+    bad = [
+        (src, dst, 64, 63, 64, pkg.F32, 16, 16, 1, -1, flags),     # cols*4 not 16-B multiple
+        (src, src + 64, 64, 64, 64, pkg.F32, 16, 16, 1, -1, flags),  # overlap
+        (src + 4, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, flags),  # misaligned
+        (src, dst, 64, 64, 64, 9, 16, 16, 1, -1, flags),           # dtype
+        (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, 2, flags),      # only_rank out of range
+        (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, src),       # flags overlap data
+    ]
+    for args in bad:
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_tile_copy(h, *args, s)
+        assert e.value.name == "EINVAL", args
+    heap.barrier()
