@@ -117,41 +117,56 @@ __device__ __forceinline__ uint32_t cvt_pack(float x, float y) {
 }
 
 // ---------------------------------------------------------------------------
+// Geometry of one output tile for 16-byte row chunks: CPR chunks per tile
+// row, RP tile rows per pass of the 256 threads.  Thread t always handles
+// chunk column t % CPR, rows t / CPR + RP * i.
+template <int BM, int BN>
+struct TileIO {
+    static constexpr int CPR = BN / 8;
+    static constexpr int RP = kThreads / CPR;
+    static constexpr int PASSES = BM / RP;
+    static constexpr int U = PASSES < 8 ? PASSES : 8;
+    static_assert(kThreads % CPR == 0 && BM % RP == 0 && PASSES % U == 0, "tile split");
+};
+
+// Bytes of the destination resource of one tile (rows_valid x cols_valid,
+// row stride ldc elements); rows beyond rows_valid fall outside it.
+__device__ __forceinline__ uint32_t tile_span(int rows_valid, int cols_valid, int ldc) {
+    return (uint32_t)(((size_t)(rows_valid - 1) * ldc + cols_valid) * 2);
+}
+
 // Copy one finished tile from the local heap to every other heap (the put of
 // Sections 4.1.1 and 4.2.2) and release its counters there.
-template <int BM, int BN>
+template <int BM, int BN, bool NT>
 __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
-    constexpr int CPR = BN / 8;                 // 16-byte chunks per tile row
-    constexpr int TOTAL = BM * CPR;
-    constexpr int PER = TOTAL / kThreads;
-    constexpr int U = PER < 8 ? PER : 8;
-    static_assert(TOTAL % kThreads == 0, "tile must split evenly over the threads");
+    using IO = TileIO<BM, BN>;
+    const int tid = threadIdx.x;
     const int m0 = tm * BM, n0 = tn * BN;
-    const uint16_t* src = p.C + (size_t)p.rank * p.N;
-    const bool nt = p.nontemporal != 0;
+    const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
+    const uint16_t* src = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
+    const uint32_t span = tile_span(rows, cols, p.ldc);
+    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+    const int c = tid % IO::CPR;
+    const uint32_t voff = (8 * c < cols)
+                              ? (uint32_t)((tid / IO::CPR) * p.ldc * 2 + c * 16)
+                              : symtile::kOOB;
+    const uint32_t pass_bytes = (uint32_t)(IO::RP * p.ldc * 2);
 #pragma unroll 1
-    for (int b = 0; b < PER; b += U) {
-        u32x4 v[U];
-        size_t off[U];
-        bool ok[U];
+    for (int b = 0; b < IO::PASSES; b += IO::U) {
+        symtile::u32x4 v[IO::U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int q = threadIdx.x + (b + u) * kThreads;
-            const int row = q / CPR, c = q % CPR;
-            ok[u] = (m0 + row < p.M) && (n0 + 8 * c < p.N);
-            off[u] = (size_t)(m0 + row) * p.ldc + (size_t)(n0 + 8 * c);
-            if (ok[u]) v[u] = symtile::ld16(src + off[u]);
-        }
+        for (int u = 0; u < IO::U; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
         for (int d = 1; d < p.world; ++d) {
             const int s = (p.rank + d) % p.world;
-            uint16_t* dst = symtile::translate(const_cast<uint16_t*>(src), p.rank, s, p.bases);
+            const symtile::rsrc_t rd =
+                symtile::make_rsrc(symtile::translate(src, p.rank, s, p.bases), span);
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (ok[u]) symtile::st16(dst + off[u], v[u], nt);
+            for (int u = 0; u < IO::U; ++u)
+                symtile::buf_st16<NT>(v[u], rd, voff, (b + u) * pass_bytes);
         }
     }
     symtile::wg_release_begin();
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
         uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
         for (int d = 1; d < p.world; ++d)
             symtile::flag_add_release(
@@ -169,11 +184,12 @@ void gas_kernel(const GasParams p) {
     constexpr int STAGE = A_BYTES + B_BYTES;
     constexpr int C_BYTES = BM * BN * 2;
     constexpr int LDS_BYTES = (2 * STAGE > C_BYTES) ? 2 * STAGE : C_BYTES;
-    constexpr int A_LD = BM * (BK / 8) / kThreads;      // A chunks per thread
-    constexpr int B_UNITS = (BN / 8) * (BK / 8);        // (n chunk, 8-row k group) pairs
-    constexpr int B_LD = (B_UNITS + kThreads - 1) / kThreads;
+    constexpr int A_INSTR = BM / 32;            // direct-to-LDS loads per wave per K tile
+    constexpr int NC = BN / 8;                  // B column chunks
+    constexpr int B_THREADS = NC * (BK / 8);    // threads staging B (8 k rows each)
     static_assert(MI >= 1 && NI >= 1 && WM % 32 == 0 && WN % 32 == 0, "unsupported tile");
-    static_assert(BM * (BK / 8) % kThreads == 0, "A tile must split evenly");
+    static_assert(B_THREADS <= kThreads && B_THREADS % 64 == 0, "B staging split");
+    using IO = TileIO<BM, BN>;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
     __shared__ int s_ok;
@@ -200,7 +216,10 @@ void gas_kernel(const GasParams p) {
             }
             __syncthreads();
             if (!s_ok) return;
-            put_tile_to_peers<BM, BN>(p, tm, tn);
+            if (p.nontemporal)
+                put_tile_to_peers<BM, BN, true>(p, tm, tn);
+            else
+                put_tile_to_peers<BM, BN, false>(p, tm, tn);
         }
         return;
     }
@@ -208,12 +227,29 @@ void gas_kernel(const GasParams p) {
     // ---------------- producer workgroups ---------------------------------
     const int G = p.gemm_wgs;
     const int KT = (p.K + BK - 1) / BK;
-    const bool nt = p.nontemporal != 0;
+
+    // A: wave w, load u fills staged rows 8*(4u+w) .. +7; lane l lands at
+    // LDS position l & 7 of row 8*(4u+w) + (l >> 3), so it fetches the
+    // global chunk that the XOR swizzle maps there.
+    const int lr = lane >> 3, lc = lane & 7;
+    const int a_chunk_even = lc ^ lr ^ wave;            // u even: (4u + w) & 7 == w
+    const int a_chunk_odd = a_chunk_even ^ 4;           // u odd:  (4u + w) & 7 == w + 4
+    const uint32_t a_row_off = (uint32_t)((8 * wave + lr) * p.lda * 2);
+    const uint32_t a_u_bytes = (uint32_t)(32 * p.lda * 2);
+    // B: thread (nc, kg) loads rows 8kg..8kg+7 of column chunk nc.
+    const int b_nc = tid % NC, b_kg = tid / NC;
+    const uint32_t b_voff = (uint32_t)(b_kg * 8 * p.ldb * 2 + b_nc * 16);
+    const uint32_t b_row_bytes = (uint32_t)(p.ldb * 2);
 
     for (int t = pid; t < p.num_tiles; t += G) {
         int tm, tn;
         tile_coords(t, G, p, tm, tn);
         const int m0 = tm * BM, n0 = tn * BN;
+        const int rows_a = min(BM, p.M - m0);
+        const symtile::rsrc_t rA =
+            symtile::make_rsrc(p.A + (size_t)m0 * p.lda, (uint32_t)(rows_a * p.lda * 2));
+        const symtile::rsrc_t rB = symtile::make_rsrc(
+            p.B + n0, p.K > 0 ? (uint32_t)((size_t)p.K * p.ldb * 2 - (size_t)n0 * 2) : 0u);
 
         f32x16_t acc[MI][NI];
 #pragma unroll
@@ -223,109 +259,108 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-        u32x4 ra[A_LD];
-        u32x4 rb[B_LD][8];
+        symtile::u32x4 rb[8];
 
-        // Global -> registers for K tile kt (zero outside the matrices).
-        auto load_tile = [&](int kt) {
+        // A straight into LDS stage `buf`; B into registers.  Chunks at
+        // k >= K read zero (offset outside the resource).
+        auto load_tile = [&](int kt, int buf) {
             const int k0 = kt * BK;
+            uint8_t* As = smem + buf * STAGE;
+            const uint32_t v_even = (k0 + 8 * a_chunk_even < p.K)
+                                        ? a_row_off + a_chunk_even * 16 : symtile::kOOB;
+            const uint32_t v_odd = (k0 + 8 * a_chunk_odd < p.K)
+                                       ? a_row_off + a_chunk_odd * 16 : symtile::kOOB;
 #pragma unroll
-            for (int u = 0; u < A_LD; ++u) {
-                const int q = tid + u * kThreads;
-                const int row = q >> 3, c = q & 7;
-                const int gr = m0 + row, gk = k0 + 8 * c;
-                ra[u] = (gr < p.M && gk < p.K)
-                            ? symtile::ld16(p.A + (size_t)gr * p.lda + gk)
-                            : u32x4{0, 0, 0, 0};
-            }
+            for (int u = 0; u < A_INSTR; ++u)
+                symtile::buf_ld16_lds(rA, As + (4 * u + wave) * 1024, (u & 1) ? v_odd : v_even,
+                                      u * a_u_bytes + k0 * 2);
+            if (tid < B_THREADS) {
+                const uint32_t kb = (uint32_t)k0 * b_row_bytes;
 #pragma unroll
-            for (int u = 0; u < B_LD; ++u) {
-                const int v = tid + u * kThreads;
-                const int nc = v % (BN / 8), kg = v / (BN / 8);
-                const int gn = n0 + 8 * nc;
-                const bool col_ok = v < B_UNITS && gn < p.N;
-#pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    const int gk = k0 + 8 * kg + r;
-                    rb[u][r] = (col_ok && gk < p.K)
-                                   ? symtile::ld16(p.B + (size_t)gk * p.ldb + gn)
-                                   : u32x4{0, 0, 0, 0};
-                }
+                for (int r = 0; r < 8; ++r)
+                    rb[r] = symtile::buf_ld16(rB, b_voff, kb + r * b_row_bytes);
             }
         };
 
-        // Registers -> LDS stage `buf`; B is transposed 8x8 on the way so
-        // that each staged B row holds 8 consecutive k of one column.
-        auto stage_tile = [&](int buf) {
-            uint8_t* As = smem + buf * STAGE;
-            uint8_t* Bs = As + A_BYTES;
+        // B registers -> LDS stage `buf`, transposed 8x8 so each staged row
+        // holds 8 consecutive k of one column.
+        auto stage_b = [&](int buf) {
+            if (tid >= B_THREADS) return;
+            uint8_t* Bs = smem + buf * STAGE + A_BYTES;
 #pragma unroll
-            for (int u = 0; u < A_LD; ++u) {
-                const int q = tid + u * kThreads;
-                const int row = q >> 3, c = q & 7;
-                *reinterpret_cast<u32x4*>(As + row * kRowBytes + ((c ^ swz(row)) << 4)) = ra[u];
-            }
+            for (int j = 0; j < 8; ++j) {
+                const int d = j >> 1;
+                symtile::u32x4 col;
 #pragma unroll
-            for (int u = 0; u < B_LD; ++u) {
-                const int v = tid + u * kThreads;
-                if (v < B_UNITS) {
-                    const int nc = v % (BN / 8), kg = v / (BN / 8);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int d = j >> 1;
-                        u32x4 col;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t x = rb[u][2 * e][d], y = rb[u][2 * e + 1][d];
-                            col[e] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u))
-                                             : ((x & 0xFFFFu) | (y << 16));
-                        }
-                        const int n = nc * 8 + j;
-                        *reinterpret_cast<u32x4*>(Bs + n * kRowBytes + ((kg ^ swz(n)) << 4)) = col;
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t x = rb[2 * e][d], y = rb[2 * e + 1][d];
+                    col[e] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
                 }
+                const int n = b_nc * 8 + j;
+                *reinterpret_cast<symtile::u32x4*>(Bs + n * kRowBytes + ((b_kg ^ swz(n)) << 4)) =
+                    col;
             }
         };
 
         // MFMAs over LDS stage `buf`.  Operands are swapped (B fragment as
         // the first source) so each lane's accumulators hold 4 consecutive
         // columns of one row of C, which makes the epilogue restage cheap.
-        auto compute_tile = [&](int buf) {
+        // Fragments are double buffered across the four k16 substeps: the
+        // LDS reads of substep s+1 are issued before the MFMAs of substep s,
+        // and scheduling fences keep the compiler from hoisting further
+        // (which would raise register pressure past the budget).
+        auto read_frags = [&](int buf, int s, symtile::u32x4 (&a)[MI], symtile::u32x4 (&b)[NI]) {
             const uint8_t* As = smem + buf * STAGE;
             const uint8_t* Bs = As + A_BYTES;
+            const int c = 2 * s + (lane >> 5);
 #pragma unroll
-            for (int s = 0; s < BK / 16; ++s) {
-                const int c = 2 * s + (lane >> 5);
-                u32x4 a[MI], b[NI];
-#pragma unroll
-                for (int i = 0; i < MI; ++i) {
-                    const int row = wm * WM + i * 32 + (lane & 31);
-                    a[i] = *reinterpret_cast<const u32x4*>(As + row * kRowBytes +
-                                                          ((c ^ swz(row)) << 4));
-                }
-#pragma unroll
-                for (int j = 0; j < NI; ++j) {
-                    const int row = wn * WN + j * 32 + (lane & 31);
-                    b[j] = *reinterpret_cast<const u32x4*>(Bs + row * kRowBytes +
-                                                          ((c ^ swz(row)) << 4));
-                }
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
-#pragma unroll
-                    for (int j = 0; j < NI; ++j) acc[i][j] = mfma32<BF16>(b[j], a[i], acc[i][j]);
+            for (int i = 0; i < MI; ++i) {
+                const int row = wm * WM + i * 32 + (lane & 31);
+                a[i] = *reinterpret_cast<const symtile::u32x4*>(As + row * kRowBytes +
+                                                               ((c ^ swz(row)) << 4));
             }
+#pragma unroll
+            for (int j = 0; j < NI; ++j) {
+                const int row = wn * WN + j * 32 + (lane & 31);
+                b[j] = *reinterpret_cast<const symtile::u32x4*>(Bs + row * kRowBytes +
+                                                               ((c ^ swz(row)) << 4));
+            }
+        };
+        auto mfmas = [&](const symtile::u32x4 (&a)[MI], const symtile::u32x4 (&b)[NI]) {
+#pragma unroll
+            for (int i = 0; i < MI; ++i)
+#pragma unroll
+                for (int j = 0; j < NI; ++j) acc[i][j] = mfma32<BF16>(b[j], a[i], acc[i][j]);
+        };
+        auto compute_tile = [&](int buf) {
+            symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
+            read_frags(buf, 0, a0, b0);
+            read_frags(buf, 1, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            read_frags(buf, 2, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            read_frags(buf, 3, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
         };
 
         if (KT > 0) {
-            load_tile(0);
-            stage_tile(0);
+            load_tile(0, 0);
+            stage_b(0);
             __syncthreads();
         }
         for (int kt = 0; kt < KT; ++kt) {
             const int cur = kt & 1;
-            if (kt + 1 < KT) load_tile(kt + 1);
+            if (kt + 1 < KT) load_tile(kt + 1, cur ^ 1);
             compute_tile(cur);
-            if (kt + 1 < KT) stage_tile(cur ^ 1);
+            if (kt + 1 < KT) stage_b(cur ^ 1);
             __syncthreads();
         }
 
@@ -350,33 +385,32 @@ void gas_kernel(const GasParams p) {
         __syncthreads();
 
         const int n_dst = (p.role == ROLE_FUSED) ? p.world : 1;
-        uint16_t* cbase = p.C + (size_t)p.rank * p.N;
-        {
-            constexpr int CPR = BN / 8;
-            constexpr int TOTAL = BM * CPR;
-            constexpr int PER = TOTAL / kThreads;
-            constexpr int U = PER < 8 ? PER : 8;
-            static_assert(TOTAL % kThreads == 0, "tile must split evenly over the threads");
+        const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
+        const uint16_t* tile_local = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
+        const uint32_t span = tile_span(rows, cols, p.ldc);
+        const int c = tid % IO::CPR, r0 = tid / IO::CPR;
+        const uint32_t voff =
+            (8 * c < cols) ? (uint32_t)(r0 * p.ldc * 2 + c * 16) : symtile::kOOB;
+        const uint32_t pass_bytes = (uint32_t)(IO::RP * p.ldc * 2);
+        const uint8_t* crow = Cs + r0 * CROW + ((c ^ (r0 & 7)) << 4);
 #pragma unroll 1
-            for (int b = 0; b < PER; b += U) {
-                u32x4 v[U];
-                size_t off[U];
-                bool ok[U];
+        for (int b = 0; b < IO::PASSES; b += IO::U) {
+            symtile::u32x4 v[IO::U];
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int q = tid + (b + u) * kThreads;
-                    const int row = q / CPR, c = q % CPR;
-                    v[u] = *reinterpret_cast<const u32x4*>(Cs + row * CROW +
-                                                          ((c ^ (row & 7)) << 4));
-                    ok[u] = (m0 + row < p.M) && (n0 + 8 * c < p.N);
-                    off[u] = (size_t)(m0 + row) * p.ldc + (size_t)(n0 + 8 * c);
-                }
-                for (int d = 0; d < n_dst; ++d) {
-                    const int s = (p.rank + d) % p.world;
-                    uint16_t* dst = symtile::translate(cbase, p.rank, s, p.bases);
+            for (int u = 0; u < IO::U; ++u)
+                v[u] = *reinterpret_cast<const symtile::u32x4*>(crow + (b + u) * IO::RP * CROW);
+            for (int d = 0; d < n_dst; ++d) {
+                const int s = (p.rank + d) % p.world;
+                const symtile::rsrc_t rd =
+                    symtile::make_rsrc(symtile::translate(tile_local, p.rank, s, p.bases), span);
+                if (p.nontemporal) {
 #pragma unroll
-                    for (int u = 0; u < U; ++u)
-                        if (ok[u]) symtile::st16(dst + off[u], v[u], nt);
+                    for (int u = 0; u < IO::U; ++u)
+                        symtile::buf_st16<true>(v[u], rd, voff, (b + u) * pass_bytes);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < IO::U; ++u)
+                        symtile::buf_st16<false>(v[u], rd, voff, (b + u) * pass_bytes);
                 }
             }
         }
@@ -396,7 +430,10 @@ template <int BM, int BN>
 __global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
     for (int t = blockIdx.x; t < p.num_tiles; t += gridDim.x) {
         const int tm = t / p.tiles_n, tn = t % p.tiles_n;
-        put_tile_to_peers<BM, BN>(p, tm, tn);
+        if (p.nontemporal)
+            put_tile_to_peers<BM, BN, true>(p, tm, tn);
+        else
+            put_tile_to_peers<BM, BN, false>(p, tm, tn);
     }
 }
 
@@ -476,7 +513,12 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         return fail(SYMTILE_EINVAL, "K, N_local, lda and ldb must be multiples of 8");
     const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16);
     if (!v) return fail(SYMTILE_EUNSUPPORTED, "tile shape not built");
-    if ((size_t)world_size * N_local > INT32_MAX) return fail(SYMTILE_EINVAL, "N too large");
+    // Buffer resources span one tile row band of A or C and the whole of B;
+    // each must stay below 2 GiB.
+    const size_t kMaxSpan = size_t(1) << 31;
+    if ((size_t)world_size * N_local * 2 * cfg.tile_m >= kMaxSpan ||
+        (size_t)lda * 2 * cfg.tile_m >= kMaxSpan || (size_t)K * ldb * 2 >= kMaxSpan)
+        return fail(SYMTILE_EINVAL, "a tile band of A or C, or B, exceeds 2 GiB");
     if (M == 0 || N_local == 0) return SYMTILE_OK;   // no tiles, nothing to publish
     if ((K > 0 && (!A || !B_shard)) || !C_gathered_local || !arrived_local)
         return fail(SYMTILE_EINVAL, "NULL pointer argument");

@@ -59,6 +59,39 @@ __device__ __forceinline__ void store(void* p, u32x4 v, int cur, int remote,
     st16(translate(p, cur, remote, bases), v, nt);
 }
 
+// ---- buffer resources ----------------------------------------------------
+// A raw buffer resource covers [base, base + bytes); a load whose offset
+// falls outside returns zero and a store there is dropped.  The kernels use
+// this instead of branches for ragged edges: an invalid lane gets kOOB as
+// its offset.  All resources here stay below 2^31 bytes, so kOOB plus any
+// scalar offset used is outside every resource.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    // dword 3 = 0x00020000: 32-bit data format, no swizzle, no index stride
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+
+// aux = 2 sets the non-temporal (streaming) hint on the store.
+template <bool NT>
+__device__ __forceinline__ void buf_st16(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, NT ? 2 : 0);
+}
+
+// 16 bytes per lane from the buffer straight into LDS: lane l of the wave
+// writes lds_base + 16 * l (lds_base is wave-uniform).
+__device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* lds_base, uint32_t voff,
+                                             uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
+}
+
 // ---- atomics with ordering and scope (Section 3.3.3) ----------------------
 // SEM is a __ATOMIC_* order, SCOPE a __HIP_MEMORY_SCOPE_* constant.
 template <int SEM, int SCOPE>

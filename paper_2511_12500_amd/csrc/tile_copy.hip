@@ -35,7 +35,9 @@ struct CopyParams {
     int tiles_c;             // tiles per matrix row of tiles
 };
 
-template <bool NT>
+// TC = 16-byte chunks per tile row when it divides the 256 threads (then
+// thread t keeps chunk column t % TC), or 0 for any other width.
+template <int TC, bool NT>
 __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p) {
     const int r = p.only_rank >= 0 ? p.only_rank : (int)blockIdx.y;
     const int dst = ((r + p.shift) % p.world + p.world) % p.world;
@@ -48,27 +50,44 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
 
     // The source is rank r's own buffer; the destination is the same
     // symmetric object translated into the heap of rank dst.
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off);
-    uint8_t* dst_local = reinterpret_cast<uint8_t*>(p.bases[r] + p.dst_off);
-    uint8_t* dstp = symtile::translate(dst_local, r, dst, p.bases);
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
+                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
+                               (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
+    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+    const symtile::rsrc_t rd = symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
 
-    const int total = nrows * p.tile_chunks;
-    for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
-        u32x4 v[kBatch];
-        size_t off[kBatch];
-        bool ok[kBatch];
+    if constexpr (TC > 0) {
+        constexpr int RP = kThreads / TC;                  // tile rows per pass
+        const int c = threadIdx.x % TC;
+        const uint32_t voff = (c < nchunks) ? (uint32_t)((threadIdx.x / TC) * p.ld_bytes + c * 16)
+                                            : symtile::kOOB;
+        const uint32_t pass_bytes = (uint32_t)(RP * p.ld_bytes);
+        const int passes = (nrows + RP - 1) / RP;
+        for (int b = 0; b < passes; b += kBatch) {
+            symtile::u32x4 v[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-            const int q = base + u * kThreads;
-            const int row = q / p.tile_chunks;
-            const int c = q - row * p.tile_chunks;
-            ok[u] = q < total && c < nchunks;
-            off[u] = (size_t)(row0 + row) * p.ld_bytes + (size_t)(chunk0 + c) * 16;
-            if (ok[u]) v[u] = symtile::ld16(src + off[u]);
+            for (int u = 0; u < kBatch; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) symtile::buf_st16<NT>(v[u], rd, voff, (b + u) * pass_bytes);
         }
+    } else {
+        const int total = nrows * p.tile_chunks;
+        for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
+            symtile::u32x4 v[kBatch];
+            uint32_t off[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-            if (ok[u]) symtile::st16(dstp + off[u], v[u], NT);
+            for (int u = 0; u < kBatch; ++u) {
+                const int q = base + u * kThreads;
+                const int row = q / p.tile_chunks, c = q - row * p.tile_chunks;
+                off[u] = (q < total && c < nchunks) ? (uint32_t)(row * p.ld_bytes + c * 16)
+                                                    : symtile::kOOB;
+                v[u] = symtile::buf_ld16(rs, off[u], 0);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) symtile::buf_st16<NT>(v[u], rd, off[u], 0);
+        }
     }
 
     // Publish: the tile is in rank dst's heap before its counter moves.
@@ -104,8 +123,8 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     const int tiles_r = (rows + tile_r - 1) / tile_r;
     const int tiles_c = (cols + tile_c - 1) / tile_c;
     const size_t ntiles = (size_t)tiles_r * tiles_c;
-    if (ld_bytes > INT32_MAX || ntiles > INT32_MAX)
-        return fail(SYMTILE_EINVAL, "matrix too large");
+    if (ld_bytes * (size_t)tile_r >= (size_t(1) << 31) || ntiles > INT32_MAX)
+        return fail(SYMTILE_EINVAL, "a tile row band exceeds 2 GiB or too many tiles");
     if (src_off > h->slot_stride || span > h->slot_stride - src_off ||
         dst_off > h->slot_stride || span > h->slot_stride - dst_off ||
         flag_off > h->slot_stride || ntiles * 4 > h->slot_stride - flag_off)
@@ -134,8 +153,13 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     int prev = -1;
     if (symtile_status st = symtile_host::set_device(h, &prev)) return st;
     const dim3 grid((unsigned)ntiles, only_rank >= 0 ? 1u : (unsigned)h->world);
-    hipLaunchKernelGGL(tile_copy_kernel<true>, grid, dim3(kThreads), 0,
-                       static_cast<hipStream_t>(s), p);
+    hipStream_t stream = static_cast<hipStream_t>(s);
+    switch (p.tile_chunks) {
+        case 16: hipLaunchKernelGGL((tile_copy_kernel<16, true>), grid, dim3(kThreads), 0, stream, p); break;
+        case 32: hipLaunchKernelGGL((tile_copy_kernel<32, true>), grid, dim3(kThreads), 0, stream, p); break;
+        case 64: hipLaunchKernelGGL((tile_copy_kernel<64, true>), grid, dim3(kThreads), 0, stream, p); break;
+        default: hipLaunchKernelGGL((tile_copy_kernel<0, true>), grid, dim3(kThreads), 0, stream, p); break;
+    }
     hipError_t e = hipGetLastError();
     (void)hipSetDevice(prev);
     if (e != hipSuccess) return symtile_host::hip_fail(e, "tile_copy_kernel launch");

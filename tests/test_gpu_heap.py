@@ -137,9 +137,9 @@ def test_atomic_add_every_order_and_scope(sem, scope):
     pkg = sym()
     heap = pkg.Heap(8, 1 << 21)
     n = 5000
-    final, old = _atomic(pkg, heap, "add", sem, scope, n, 0, 7)
-    # thread t adds t: final = 7 + n(n-1)/2; the observed olds are all distinct
-    assert final == (7 + n * (n - 1) // 2) % 2 ** 32
+    final, old = _atomic(pkg, heap, "add", sem, scope, n, 1, 7)
+    # thread t adds 1 + t > 0: final = 7 + n + n(n-1)/2 and every observed old differs
+    assert final == (7 + n + n * (n - 1) // 2) % 2 ** 32
     assert len(np.unique(old)) == n
 
 
