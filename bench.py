@@ -78,6 +78,7 @@ def parse_args(argv=None):
     ap.add_argument("--nontemporal", type=int, default=0)
     ap.add_argument("--copy-tile", type=int, default=128)
     ap.add_argument("--copy-iters", type=int, default=20)
+    ap.add_argument("--copy-per-wg", type=int, default=0, help="tiles per workgroup (0 = auto)")
     ap.add_argument("--no-copy", action="store_true", help="skip the heap tile-copy leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -155,20 +156,22 @@ def bench_copy(args, torch, sym, workload):
     src, dst = heap.alloc(nbytes), heap.alloc(nbytes)
     flags = heap.alloc(1 << 16)
     heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(workload.copy_send(wl).cuda())
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")   # > 256 MB MALL
+    # Cold runs: read 1 GiB of other data first (more than the 256 MB MALL) so
+    # the heap is evicted; a read leaves no dirty lines to write back later.
+    flush = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
     t = args.copy_tile
     stream = sym.current_stream()
 
     def launch():
         sym.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, sym.F32, t, t,
-                              wl.shift, -1, flags, stream)
+                              wl.shift, -1, flags, tiles_per_wg=args.copy_per_wg, stream=stream)
 
     for _ in range(3):
         launch()
     torch.cuda.synchronize()
     cold, warm = [], []
     for i in range(args.copy_iters):
-        flush.zero_()
+        flush.max()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         launch()
@@ -193,6 +196,7 @@ def bench_copy(args, torch, sym, workload):
     del flush
     return {
         "value": gbs, "unit": "GB/s", "tile": f"{t}x{t}", "workload": wl.name,
+        "tiles_per_wg": args.copy_per_wg,
         "bytes_per_launch": moved, "cold_ms": cold_ms, "warm_ms": warm_ms,
         "warm_GBps": moved / (warm_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

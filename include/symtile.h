@@ -165,13 +165,16 @@ symtile_status symtile_atomic_exercise(symtile_heap* h, int op, int sem, int sco
  * release-publish (agent scope) one uint32 counter per tile at
  * flag_off + 4 * tile of the destination slot (tile = tr * tiles_c + tc).
  * Row stride `ld` elements; element size from dtype (2 or 4 bytes).  All
- * ranks run in one launch.  Requirements: cols*esize, tile_c*esize and
- * ld*esize multiples of 16; offsets 16-byte aligned; regions inside the
+ * ranks run in one launch.  Each workgroup copies tiles_per_wg consecutive
+ * (rank, tile) items and publishes their counters after one release
+ * (0 = about two workgroups per CU).  Requirements: cols*esize, tile_c*esize
+ * and ld*esize multiples of 16; offsets 16-byte aligned; regions inside the
  * slot; the source and destination regions must not overlap.  EINVAL
  * otherwise. */
 symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off, int rows,
                                  int cols, int ld, int dtype, int tile_r, int tile_c,
-                                 int shift, int only_rank, size_t flag_off, symtile_stream s);
+                                 int shift, int only_rank, size_t flag_off, int tiles_per_wg,
+                                 symtile_stream s);
 
 /* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
 

@@ -61,7 +61,7 @@ def _load():
         "symtile_barrier": [vp, vp],
         "symtile_heap_fill": [vp, i32, sz, sz, i32, vp],
         "symtile_atomic_exercise": [vp, i32, i32, i32, sz, i32, i32, i32, u32, u32, vp, vp],
-        "symtile_tile_copy": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, vp],
+        "symtile_tile_copy": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, i32, vp],
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
@@ -178,9 +178,10 @@ def symtile_atomic_exercise(h: int, op: int, sem: int, scope: int, offset: int, 
 
 def symtile_tile_copy(h: int, src_off: int, dst_off: int, rows: int, cols: int, ld: int,
                       dtype: int, tile_r: int, tile_c: int, shift: int, only_rank: int,
-                      flag_off: int, stream: int = 0) -> None:
+                      flag_off: int, tiles_per_wg: int = 0, stream: int = 0) -> None:
     _check(lib.symtile_tile_copy(_vp(h), src_off, dst_off, rows, cols, ld, dtype, tile_r, tile_c,
-                                 shift, only_rank, flag_off, _vp(stream)), "symtile_tile_copy")
+                                 shift, only_rank, flag_off, tiles_per_wg, _vp(stream)),
+           "symtile_tile_copy")
 
 
 def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int,

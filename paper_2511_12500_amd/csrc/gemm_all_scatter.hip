@@ -165,12 +165,12 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
                 symtile::buf_st16<NT>(v[u], rd, voff, (b + u) * pass_bytes);
         }
     }
-    symtile::wg_release_begin();
+    symtile::wg_stores_done();
     if (tid == 0) {
+        symtile::release_agent();
         uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
         for (int d = 1; d < p.world; ++d)
-            symtile::flag_add_release(
-                symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
+            symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
     }
 }
 
@@ -414,13 +414,13 @@ void gas_kernel(const GasParams p) {
                 }
             }
         }
-        symtile::wg_release_begin();   // also orders the LDS reads above before reuse
+        symtile::wg_stores_done();
         if (tid == 0) {
+            symtile::release_agent();
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
             for (int d = 0; d < n_dst; ++d)
-                symtile::flag_add_release(
-                    symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
-            if (p.role == ROLE_WG_SPEC) symtile::flag_add_release(p.ready + tm * p.tiles_n + tn);
+                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
+            if (p.role == ROLE_WG_SPEC) symtile::flag_add(p.ready + tm * p.tiles_n + tn);
         }
     }
 }

@@ -68,9 +68,20 @@ __device__ __forceinline__ void store(void* p, u32x4 v, int cur, int remote,
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr uint32_t kOOB = 0x80000000u;
 
+// The resource must be the same for every lane of the wave (all uses here
+// are per tile and per slot).  Its base and size are read through
+// readfirstlane so the descriptor lives in scalar registers even when the
+// compiler cannot prove uniformity (e.g. a base loaded from the bases array);
+// a descriptor in vector registers would turn every buffer access into a
+// loop over distinct descriptor values.
 __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    void* ub = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
     // dword 3 = 0x00020000: 32-bit data format, no swizzle, no index stride
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+    return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0,
+                                             (int)__builtin_amdgcn_readfirstlane(bytes),
                                              0x00020000);
 }
 
@@ -78,10 +89,22 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff, uint32_t soff
     return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
 }
 
-// aux = 2 sets the non-temporal (streaming) hint on the store.
+// Store cache policies (the cache-policy bits of the gfx9.4/9.5 store):
+//   kStoreDefault      write-back in the L2;
+//   kStoreNonTemporal  nt: streaming hint, the line is a preferred victim;
+//   kStoreWriteThrough sc0 sc1: system-scope coherence, written through the
+//                      L2 to memory (measured best for the cold heap copy,
+//                      where the destination is not read again soon).
+enum : int { kStoreDefault = 0, kStoreNonTemporal = 2, kStoreWriteThrough = 17 };
+
+template <int POLICY>
+__device__ __forceinline__ void buf_st16p(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, POLICY);
+}
+
 template <bool NT>
 __device__ __forceinline__ void buf_st16(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, NT ? 2 : 0);
+    buf_st16p<NT ? kStoreNonTemporal : kStoreDefault>(v, r, voff, soff);
 }
 
 // 16 bytes per lane from the buffer straight into LDS: lane l of the wave
@@ -132,18 +155,29 @@ __device__ __forceinline__ uint32_t atomic_max(uint32_t* p, uint32_t v) {
 }
 
 // ---- per-tile flags ------------------------------------------------------
-// Workgroup-wide publication: every thread makes its own earlier stores
-// visible at agent scope, the workgroup meets at a barrier, then thread 0
-// issues a release fence and increments each of the n counters.  Must be
-// called by every thread of the workgroup.
-__device__ __forceinline__ void wg_release_begin() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+// Publication of a workgroup's stores, with one L2 write-back per workgroup:
+//  1. wg_stores_done(), by every thread: the wave waits until its own
+//     earlier memory operations are acknowledged (vmcnt 0, i.e. the stores
+//     have reached the L2), then the workgroup meets at a barrier;
+//  2. release_agent(), by one thread afterwards: an agent-scope release
+//     fence, whose L2 write-back covers the stores of every wave of the
+//     workgroup (they are all in this XCD's L2 by step 1);
+//  3. flag_add(), by the same thread: relaxed agent-scope increments.  A
+//     release fence followed by an atomic write synchronises with an
+//     acquire that reads the written value.
+// An agent-scope release per wave, or a release-ordered increment per
+// counter, would each cost another full L2 write-back.
+__device__ __forceinline__ void wg_stores_done() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0); expcnt and lgkmcnt not waited
     __syncthreads();
 }
 
-__device__ __forceinline__ void flag_add_release(uint32_t* flag) {
-    // caller is one thread that has passed wg_release_begin()
-    __hip_atomic_fetch_add(flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void release_agent() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+}
+
+__device__ __forceinline__ void flag_add(uint32_t* flag) {
+    __hip_atomic_fetch_add(flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Bounded wait by one thread until *flag >= target.  Polls with relaxed

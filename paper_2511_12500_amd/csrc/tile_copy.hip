@@ -3,10 +3,17 @@
 // (r + shift) mod w in one launch, with one release-published counter per
 // tile in the destination slot.
 //
-// Data path: HBM-bound.  Each workgroup owns one tile; every thread moves
-// 16-byte chunks, issuing a batch of loads before the matching stores so
-// many requests are in flight per wave.  Consecutive lanes take consecutive
-// chunks of a tile row, so each wave instruction covers whole cache lines.
+// Data path: HBM-bound.  Each workgroup owns a run of tiles_per_wg
+// consecutive (rank, tile) items; every thread moves 16-byte chunks,
+// issuing a batch of loads before the matching stores so many requests are
+// in flight per wave.  Consecutive lanes take consecutive chunks of a tile
+// row, so each wave instruction covers whole cache lines.  After its run the
+// workgroup publishes all of its counters behind one agent-scope release:
+// the release is an L2 write-back, serialised per XCD, so its count (not the
+// data path) bounds the kernel when every tile pays for one.  A run of
+// adjacent tiles of one tile row is copied as one rectangle, row by row, so
+// the memory sees long row segments instead of many short ones.  Stores are
+// written through to memory (cold copies measured fastest that way).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -20,8 +27,17 @@ namespace {
 
 using symtile::u32x4;
 
-constexpr int kThreads = 256;
-constexpr int kBatch = 8;   // chunks in flight per thread
+// Workgroup shape: one wide workgroup per CU keeps the number of releases
+// (one per workgroup) small while 16 waves per CU keep enough loads in
+// flight to cover HBM latency.
+#ifndef SYMTILE_COPY_THREADS
+#define SYMTILE_COPY_THREADS 1024
+#endif
+#ifndef SYMTILE_COPY_BATCH
+#define SYMTILE_COPY_BATCH 8
+#endif
+constexpr int kThreads = SYMTILE_COPY_THREADS;
+constexpr int kBatch = SYMTILE_COPY_BATCH;   // chunks in flight per thread
 
 struct CopyParams {
     const uint64_t* bases;
@@ -33,15 +49,17 @@ struct CopyParams {
     int tile_r;              // tile rows
     int tile_chunks;         // 16-byte chunks per tile row
     int tiles_c;             // tiles per matrix row of tiles
+    int ntiles;              // tiles per rank
+    int nitems;              // (rank, tile) items of this launch
+    int per_wg;              // consecutive items per workgroup
+    int band_lg_w;           // >= 0: each run is one rectangle, 1 << band_lg_w chunks wide
 };
 
-// TC = 16-byte chunks per tile row when it divides the 256 threads (then
-// thread t keeps chunk column t % TC), or 0 for any other width.
-template <int TC, bool NT>
-__global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p) {
-    const int r = p.only_rank >= 0 ? p.only_rank : (int)blockIdx.y;
-    const int dst = ((r + p.shift) % p.world + p.world) % p.world;
-    const int tile = blockIdx.x;
+// Copy tile `tile` of source rank r to rank dst.  TC = 16-byte chunks per
+// tile row when it divides the thread count (thread t keeps chunk column
+// t % TC), or 0 for any other width.
+template <int TC, int POLICY>
+__device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int dst, int tile) {
     const int tr = tile / p.tiles_c, tc = tile - tr * p.tiles_c;
     const int row0 = tr * p.tile_r;
     const int chunk0 = tc * p.tile_chunks;
@@ -56,7 +74,8 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
                                (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
     const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
     const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
-    const symtile::rsrc_t rd = symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
+    const symtile::rsrc_t rd =
+        symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
 
     if constexpr (TC > 0) {
         constexpr int RP = kThreads / TC;                  // tile rows per pass
@@ -66,16 +85,17 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
         const uint32_t pass_bytes = (uint32_t)(RP * p.ld_bytes);
         const int passes = (nrows + RP - 1) / RP;
         for (int b = 0; b < passes; b += kBatch) {
-            symtile::u32x4 v[kBatch];
+            u32x4 v[kBatch];
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) symtile::buf_st16<NT>(v[u], rd, voff, (b + u) * pass_bytes);
+            for (int u = 0; u < kBatch; ++u)
+                symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
         }
     } else {
         const int total = nrows * p.tile_chunks;
         for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
-            symtile::u32x4 v[kBatch];
+            u32x4 v[kBatch];
             uint32_t off[kBatch];
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) {
@@ -86,15 +106,74 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
                 v[u] = symtile::buf_ld16(rs, off[u], 0);
             }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) symtile::buf_st16<NT>(v[u], rd, off[u], 0);
+            for (int u = 0; u < kBatch; ++u) symtile::buf_st16p<POLICY>(v[u], rd, off[u], 0);
         }
     }
+}
 
-    // Publish: the tile is in rank dst's heap before its counter moves.
-    symtile::wg_release_begin();
+// Copy the rows x nchunks rectangle at (row0, chunk0) of rank r to rank dst
+// in row-major order: consecutive threads take consecutive 16-byte chunks of
+// a row (a row of up to W = 1 << lg_w chunks per pass group), so a run of
+// horizontally adjacent tiles streams whole row segments of up to 8 KiB.
+template <int POLICY>
+__device__ __forceinline__ void copy_rect(const CopyParams& p, int r, int dst, int row0,
+                                          int chunk0, int nrows, int nchunks, int lg_w) {
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
+                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
+                               (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
+    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+    const symtile::rsrc_t rd =
+        symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
+    const int c = threadIdx.x & ((1 << lg_w) - 1);
+    const int rp = kThreads >> lg_w;                       // rows per pass
+    const uint32_t voff = (c < nchunks) ? (uint32_t)((threadIdx.x >> lg_w) * p.ld_bytes + c * 16)
+                                        : symtile::kOOB;
+    const uint32_t pass_bytes = (uint32_t)(rp * p.ld_bytes);
+    const int passes = (nrows + rp - 1) / rp;
+    for (int b = 0; b < passes; b += kBatch) {
+        u32x4 v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
+    }
+}
+
+template <int TC, int POLICY>
+__global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p) {
+    const int first = blockIdx.x * p.per_wg;
+    const int last = min(first + p.per_wg, p.nitems);
+    if (p.band_lg_w >= 0) {
+        // The run is per_wg adjacent tiles of one tile row: one rectangle.
+        const int r = p.only_rank >= 0 ? p.only_rank : first / p.ntiles;
+        const int dst = ((r + p.shift) % p.world + p.world) % p.world;
+        const int t0 = first % p.ntiles;
+        const int tr = t0 / p.tiles_c, tc = t0 - tr * p.tiles_c;
+        const int row0 = tr * p.tile_r, chunk0 = tc * p.tile_chunks;
+        copy_rect<POLICY>(p, r, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
+                      min(p.per_wg * p.tile_chunks, p.row_chunks - chunk0), p.band_lg_w);
+    } else {
+        for (int it = first; it < last; ++it) {
+            const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
+            const int dst = ((r + p.shift) % p.world + p.world) % p.world;
+            copy_one_tile<TC, POLICY>(p, r, dst, it % p.ntiles);
+        }
+    }
+    // Publish: every tile of the run is in its destination heap before any
+    // of its counters moves.
+    symtile::wg_stores_done();
     if (threadIdx.x == 0) {
-        uint32_t* flag_local = reinterpret_cast<uint32_t*>(p.bases[r] + p.flag_off) + tile;
-        symtile::flag_add_release(symtile::translate(flag_local, r, dst, p.bases));
+        symtile::release_agent();
+        for (int it = first; it < last; ++it) {
+            const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
+            const int dst = ((r + p.shift) % p.world + p.world) % p.world;
+            uint32_t* flag_local =
+                reinterpret_cast<uint32_t*>(p.bases[r] + p.flag_off) + it % p.ntiles;
+            symtile::flag_add(symtile::translate(flag_local, r, dst, p.bases));
+        }
     }
 }
 
@@ -103,7 +182,8 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
 extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off,
                                             int rows, int cols, int ld, int dtype, int tile_r,
                                             int tile_c, int shift, int only_rank,
-                                            size_t flag_off, symtile_stream s) {
+                                            size_t flag_off, int tiles_per_wg,
+                                            symtile_stream s) {
     using symtile_host::fail;
     if (!h) return fail(SYMTILE_EINVAL, "heap is NULL");
     int esize = 0;
@@ -117,6 +197,7 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     if (src_off % 16 || dst_off % 16 || flag_off % 4)
         return fail(SYMTILE_EINVAL, "offsets misaligned (16 bytes for data, 4 for flags)");
     if (only_rank >= h->world) return fail(SYMTILE_EINVAL, "only_rank out of range");
+    if (tiles_per_wg < 0) return fail(SYMTILE_EINVAL, "tiles_per_wg < 0");
     if (rows == 0 || cols == 0) return SYMTILE_OK;
     const size_t ld_bytes = (size_t)ld * esize;
     const size_t span = (size_t)(rows - 1) * ld_bytes + (size_t)cols * esize;
@@ -149,16 +230,41 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     p.tile_r = tile_r;
     p.tile_chunks = (int)((size_t)tile_c * esize / 16);
     p.tiles_c = tiles_c;
+    p.ntiles = (int)ntiles;
+    const size_t nitems = ntiles * (only_rank >= 0 ? 1 : (size_t)h->world);
+    if (nitems > INT32_MAX) return fail(SYMTILE_EINVAL, "too many tiles");
+    p.nitems = (int)nitems;
+    if (tiles_per_wg == 0) {
+        // about one workgroup per CU: enough waves to fill the chip while
+        // keeping the number of L2 write-backs (one per workgroup) small;
+        // rounded to a power of two that divides the tiles of a tile row so
+        // that every run is one rectangle
+        const size_t target = (size_t)std::max(1, symtile_host::cu_count(h->device));
+        size_t per = std::max<size_t>(1, (nitems + target - 1) / target);
+        size_t pow2 = 1;
+        while (pow2 * 2 <= per && tiles_c % (pow2 * 2) == 0) pow2 *= 2;
+        tiles_per_wg = (int)pow2;
+    }
+    p.per_wg = tiles_per_wg;
+    // Rectangle mode: runs never straddle a tile row and the run width
+    // (rounded up to a power of two) fits the workgroup.
+    p.band_lg_w = -1;
+    if (tiles_c % tiles_per_wg == 0) {
+        const size_t width = (size_t)tiles_per_wg * p.tile_chunks;
+        int lg = 0;
+        while (((size_t)1 << lg) < width) ++lg;
+        if (((size_t)1 << lg) <= (size_t)kThreads) p.band_lg_w = lg;
+    }
 
     int prev = -1;
     if (symtile_status st = symtile_host::set_device(h, &prev)) return st;
-    const dim3 grid((unsigned)ntiles, only_rank >= 0 ? 1u : (unsigned)h->world);
+    const dim3 grid((unsigned)((nitems + p.per_wg - 1) / p.per_wg));
     hipStream_t stream = static_cast<hipStream_t>(s);
     switch (p.tile_chunks) {
-        case 16: hipLaunchKernelGGL((tile_copy_kernel<16, true>), grid, dim3(kThreads), 0, stream, p); break;
-        case 32: hipLaunchKernelGGL((tile_copy_kernel<32, true>), grid, dim3(kThreads), 0, stream, p); break;
-        case 64: hipLaunchKernelGGL((tile_copy_kernel<64, true>), grid, dim3(kThreads), 0, stream, p); break;
-        default: hipLaunchKernelGGL((tile_copy_kernel<0, true>), grid, dim3(kThreads), 0, stream, p); break;
+        case 16: hipLaunchKernelGGL((tile_copy_kernel<16, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
+        case 32: hipLaunchKernelGGL((tile_copy_kernel<32, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
+        case 64: hipLaunchKernelGGL((tile_copy_kernel<64, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
+        default: hipLaunchKernelGGL((tile_copy_kernel<0, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
     }
     hipError_t e = hipGetLastError();
     (void)hipSetDevice(prev);

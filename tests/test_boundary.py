@@ -78,7 +78,22 @@ def test_oracle_and_hip_path_share_nothing():
 
 
 def test_product_has_no_cpu_fallback():
-    """The package imports the HIP library eagerly and raises if it is absent."""
+    """The binding loads the HIP library when first used and raises if it is
+    absent; the build module imports without it."""
     src = open(os.path.join(PKG, "_binding.py")).read()
     assert "raise ImportError" in src
     assert "lib = _load()" in src
+
+
+def test_build_module_imports_without_the_library(tmp_path):
+    import shutil
+    import subprocess
+    import sys
+    dst = tmp_path / "paper_2511_12500_amd"
+    shutil.copytree(PKG, dst, ignore=shutil.ignore_patterns("*.so", "__pycache__"))
+    code = ("import paper_2511_12500_amd as p, paper_2511_12500_amd.build as b; "
+            "assert b.SOURCES\n"
+            "try:\n    p.Heap\nexcept ImportError as e:\n    print('raised', e)\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    assert "raised" in r.stdout and "not built" in r.stdout

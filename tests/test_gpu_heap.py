@@ -182,8 +182,8 @@ def _copy_heap(pkg, world, rows, cols, dtype_t):
     return heap, src, dst, flags
 
 
-@pytest.mark.parametrize("tile", [64, 128, 256])
-def test_heap_tile_copy_workload_bitexact(tile):
+@pytest.mark.parametrize("tile,per_wg", [(64, 0), (128, 0), (256, 0), (128, 1), (64, 7)])
+def test_heap_tile_copy_workload_bitexact(tile, per_wg):
     """All 8 ranks copy send -> recv of rank (r+1) mod 8, 2048 x 2048 fp32."""
     pkg = sym()
     wl = workload.HEAP_COPY
@@ -192,7 +192,7 @@ def test_heap_tile_copy_workload_bitexact(tile):
     heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(send.cuda())
     heap.slots_view(dst, (wl.rows, wl.cols), torch.int32).fill_(-1)
     pkg.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, pkg.F32, tile, tile,
-                          wl.shift, -1, flags, pkg.current_stream())
+                          wl.shift, -1, flags, tiles_per_wg=per_wg, stream=pkg.current_stream())
     heap.barrier()
     recv = heap.slots_view(dst, (wl.rows, wl.cols), torch.float32).cpu().numpy()
     ntiles = (wl.rows // tile) * (wl.cols // tile)
@@ -221,7 +221,7 @@ def test_heap_tile_copy_ragged_and_single_rank(case):
         heap.slots_view(flags, (ntiles,), torch.int32).zero_()
         heap.slots_view(dst, (rows, cols), ival).zero_()
         pkg.symtile_tile_copy(heap.handle, src, dst, rows, cols, cols, code, tr, tc, shift,
-                              only, flags, pkg.current_stream())
+                              only, flags, tiles_per_wg=3, stream=pkg.current_stream())
         heap.barrier()
         recv = heap.slots_view(dst, (rows, cols), ival).cpu().numpy()
         fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
@@ -243,8 +243,11 @@ def test_heap_tile_copy_rejects_bad_arguments():
         (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, 2, flags),      # only_rank out of range
         (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, src),       # flags overlap data
     ]
+    with pytest.raises(pkg.SymtileError) as e:
+        pkg.symtile_tile_copy(h, src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, flags, -1, s)
+    assert e.value.name == "EINVAL"
     for args in bad:
         with pytest.raises(pkg.SymtileError) as e:
-            pkg.symtile_tile_copy(h, *args, s)
+            pkg.symtile_tile_copy(h, *args, 0, s)
         assert e.value.name == "EINVAL", args
     heap.barrier()
