@@ -45,17 +45,19 @@ def sources_sha(paths) -> str:
 
 def counter_traffic(name: str, sources) -> float | None:
     """HBM bytes per launch from a committed rocprofv3 --pmc summary
-    ``profiles/<name>``: lines ``bytes_per_dispatch: X`` and ``source_sha: H``.
-    None when absent or when the kernel source changed since it was taken."""
+    ``profiles/<name>`` (written by ``python -m paper_2511_12500_amd.profiling``):
+    lines ``- bytes_per_dispatch: X`` and ``- source_sha: H``.  None when absent
+    or when the kernel source changed since the counters were taken."""
     path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
         return None
     fields = {}
     with open(path) as f:
         for line in f:
-            if ":" in line:
-                k, v = line.split(":", 1)
-                fields[k.strip().lstrip("- ").strip("`")] = v.strip().strip("`")
+            if line.startswith("- ") and ":" in line:
+                k, v = line[2:].split(":", 1)
+                v = v.strip().split()
+                fields[k.strip()] = v[0] if v else ""
     if fields.get("source_sha") != sources_sha(sources):
         return None
     try:
@@ -70,12 +72,12 @@ def parse_args(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
-    ap.add_argument("--variant", default="wg_spec", choices=["bulk_sync", "fused_seq", "wg_spec"])
+    ap.add_argument("--variant", default="fused_seq", choices=["bulk_sync", "fused_seq", "wg_spec"])
     ap.add_argument("--tile", default="256x256")
     ap.add_argument("--gemm-wgs", type=int, default=0)
     ap.add_argument("--copy-wgs", type=int, default=0)
     ap.add_argument("--group-m", type=int, default=0)
-    ap.add_argument("--nontemporal", type=int, default=0)
+    ap.add_argument("--nontemporal", type=int, default=1)
     ap.add_argument("--copy-tile", type=int, default=128)
     ap.add_argument("--copy-iters", type=int, default=20)
     ap.add_argument("--copy-per-wg", type=int, default=0, help="tiles per workgroup (0 = auto)")
@@ -83,6 +85,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--calibrate-traffic", action="store_true",
+                    help="also run a plain 256 MiB device copy (known bytes) for counter runs")
     return ap.parse_args(argv)
 
 
@@ -129,7 +133,7 @@ def bench_gas(args, torch, sym, workload):
     kernel_s = (sum(per_launch_ms) / K) * 1e-3
     achieved = flops / kernel_s / 1e12
     peak = PEAK_MFMA_TFLOPS[wl.dtype]
-    traffic = counter_traffic(f"gas_kernel_{wl.name}_pmc.txt", KERNEL_SOURCES)
+    traffic = counter_traffic(f"gas_kernel_{wl.name}.md", KERNEL_SOURCES)
     res = {
         "value": flops / (ms_per_step * 1e-3) / 1e12,
         "ms_per_step": ms_per_step,
@@ -191,7 +195,7 @@ def bench_copy(args, torch, sym, workload):
     cold_ms = sum(cold) / len(cold)
     warm_ms = sum(warm) / len(warm)
     gbs = moved / (cold_ms * 1e-3) / 1e9
-    traffic = counter_traffic(f"tile_copy_kernel_{wl.name}_t{t}_pmc.txt", COPY_SOURCES)
+    traffic = counter_traffic(f"tile_copy_kernel_{wl.name}_t{t}.md", COPY_SOURCES)
     heap.close()
     del flush
     return {
@@ -207,26 +211,24 @@ def bench_copy(args, torch, sym, workload):
 
 def cpu_baseline(args, wl, A, B, workload):
     """The oracle (GEMM + placement into every slot + counters) timed on the
-    host cores on the first rows of the same workload; TFLOP/s."""
+    host cores on the first rows of the same workload, repeated until about
+    --cpu-seconds of work; TFLOP/s."""
     import oracle
     Ab, Bb = workload.bits(A), workload.bits(B)
     threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
-
-    def run(rows):
-        st = oracle.GatheredState(wl.world, rows, wl.N_local, 256, 256)
+    rows = min(512, wl.M)                 # bounds the oracle's gathered state (~0.6 GB)
+    st = oracle.GatheredState(wl.world, rows, wl.N_local, 256, 256)
+    done, total = 0, 0.0
+    while total < args.cpu_seconds and done < 64:
         t0 = time.perf_counter()
         oracle.gemm_all_scatter(st, Ab[:rows], Bb, wl.dtype, 0)
-        return time.perf_counter() - t0
-
-    rows = 64
-    dt = run(rows)
-    per_row = dt / rows
-    rows = int(max(64, min(1024, args.cpu_seconds / max(per_row, 1e-9))))
-    dt = run(rows)
-    flops = 2.0 * rows * wl.N_local * wl.K
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"rows 0..{rows - 1} of A (of {wl.M}) for rank 0's shard: fp32 GEMM + "
-                      f"placement into {wl.world} slots + counters, {dt:.2f} s"}
+        total += time.perf_counter() - t0
+        done += 1
+    flops = 2.0 * rows * wl.N_local * wl.K * done
+    return {"value": flops / total / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"rows 0..{rows - 1} of A (of {wl.M}) against rank 0's shard "
+                      f"[{wl.K}, {wl.N_local}]: fp32 GEMM + placement into {wl.world} slots + "
+                      f"counters, {done} repetitions, {total:.1f} s"}
 
 
 def main(argv=None):
@@ -265,6 +267,13 @@ def main(argv=None):
         line["tile_copy"] = bench_copy(args, torch, sym, workload)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args, wl, A, B, workload)
+    if args.calibrate_traffic:
+        # a plain copy kernel of known size: 256 MiB read + 256 MiB written
+        x = torch.ones(1 << 28, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
     print(json.dumps(line), flush=True)
     return 0
 

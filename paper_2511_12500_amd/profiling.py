@@ -1,0 +1,115 @@
+"""Summaries of rocprofv3 output for the kernels of this library.
+
+Turns a ``--kernel-trace --stats`` kernel_stats CSV and two ``--pmc`` runs
+(FETCH_SIZE, then WRITE_SIZE; KiB per dispatch) into a short text summary:
+average launch duration of one kernel, and its memory traffic per launch.
+The counters are calibrated against a plain device copy of known size that
+ran in the same process (``bench.py --calibrate-traffic``): each counter is
+scaled by known_bytes / counter_value(copy), so the figure is in bytes even
+if the counter's unit or coverage differs from its nominal KiB.
+
+    python -m paper_2511_12500_amd.profiling \\
+        --trace DIR/run_kernel_stats.csv --fetch DIR2/run_counter_collection.csv \\
+        --write DIR3/run_counter_collection.csv --kernel gas_kernel \\
+        --calib direct_copy --calib-bytes 268435456 --sources a.hip b.h \\
+        --command "..." --out profiles/NAME.md
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import re
+import statistics
+import sys
+
+
+def sources_sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def trace_stats(path: str, kernel: str) -> dict:
+    """Calls and durations (ns) of the first kernel whose name matches."""
+    rx = re.compile(kernel)
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if rx.search(row["Name"]):
+                return {"name": row["Name"], "calls": int(row["Calls"]),
+                        "avg_ns": float(row["AverageNs"]), "min_ns": float(row["MinNs"]),
+                        "max_ns": float(row["MaxNs"])}
+    raise KeyError(f"no kernel matching {kernel!r} in {path}")
+
+
+def counter_per_dispatch(path: str, counter: str, kernel: str) -> tuple[float, int, str]:
+    """Median over matching dispatches of the counter summed over instances."""
+    rx = re.compile(kernel)
+    per = {}
+    name = ""
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if row["Counter_Name"] != counter or not rx.search(row["Kernel_Name"]):
+                continue
+            name = row["Kernel_Name"]
+            per[row["Dispatch_Id"]] = per.get(row["Dispatch_Id"], 0.0) + float(row["Counter_Value"])
+    if not per:
+        raise KeyError(f"no {counter} for kernel {kernel!r} in {path}")
+    return statistics.median(per.values()), len(per), name
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--kernel", required=True, help="regex of the kernel to summarise")
+    ap.add_argument("--calib", default="direct_copy", help="regex of the calibration copy")
+    ap.add_argument("--calib-bytes", type=float, default=float(1 << 28),
+                    help="bytes the calibration copy reads (and writes)")
+    ap.add_argument("--algorithmic-bytes", type=float, default=None)
+    ap.add_argument("--sources", nargs="*", default=[])
+    ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--title", default="")
+    ap.add_argument("--out", required=True)
+    a = ap.parse_args(argv)
+
+    t = trace_stats(a.trace, a.kernel)
+    lines = [f"# {a.title or t['name']}", "", "Produced by:", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", f"- kernel: `{t['name']}`",
+              f"- calls: {t['calls']}",
+              f"- avg_ns: {t['avg_ns']:.0f}",
+              f"- min_ns: {t['min_ns']:.0f}",
+              f"- max_ns: {t['max_ns']:.0f}"]
+    if a.fetch and a.write:
+        fk, n_f, _ = counter_per_dispatch(a.fetch, "FETCH_SIZE", a.kernel)
+        wk, n_w, _ = counter_per_dispatch(a.write, "WRITE_SIZE", a.kernel)
+        cf, _, _ = counter_per_dispatch(a.fetch, "FETCH_SIZE", a.calib)
+        cw, _, _ = counter_per_dispatch(a.write, "WRITE_SIZE", a.calib)
+        f_scale = a.calib_bytes / cf
+        w_scale = a.calib_bytes / cw
+        fetch_b, write_b = fk * f_scale, wk * w_scale
+        lines += ["",
+                  f"- FETCH_SIZE per dispatch (counter units): {fk:.0f} (median of {n_f})",
+                  f"- WRITE_SIZE per dispatch (counter units): {wk:.0f} (median of {n_w})",
+                  f"- calibration copy of {a.calib_bytes:.0f} B: FETCH_SIZE {cf:.0f}, "
+                  f"WRITE_SIZE {cw:.0f} -> scale {f_scale:.2f} / {w_scale:.2f} B per unit",
+                  f"- fetch_bytes_per_dispatch: {fetch_b:.0f}",
+                  f"- write_bytes_per_dispatch: {write_b:.0f}",
+                  f"- bytes_per_dispatch: {fetch_b + write_b:.0f}"]
+        if a.algorithmic_bytes:
+            lines.append(f"- algorithmic_bytes_per_dispatch: {a.algorithmic_bytes:.0f} "
+                         f"(counters / algorithmic = {(fetch_b + write_b) / a.algorithmic_bytes:.2f})")
+    if a.sources:
+        lines += ["", f"- source_sha: {sources_sha(a.sources)}  (of: {' '.join(a.sources)})"]
+    with open(a.out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
