@@ -73,6 +73,8 @@ typedef struct {
                              raises SYMTILE_ETIMEOUT; 0 = 1<<22 */
     int nontemporal;      /* 1: streaming (non-temporal) stores of the output */
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
+    int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
+                             (8 for 256x256, 4 otherwise) */
 } symtile_gas_config;
 
 /* ---- heap (Section 3.2: constructor steps 3 and 6, host API table) -------- */

@@ -38,6 +38,7 @@ class GasConfig(ctypes.Structure):
         ("spin_limit", ctypes.c_uint32),
         ("nontemporal", ctypes.c_int),
         ("group_m", ctypes.c_int),
+        ("waves_per_wg", ctypes.c_int),
     ]
 
 

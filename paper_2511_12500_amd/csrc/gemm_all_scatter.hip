@@ -118,15 +118,15 @@ __device__ __forceinline__ uint32_t cvt_pack(float x, float y) {
 
 // ---------------------------------------------------------------------------
 // Geometry of one output tile for 16-byte row chunks: CPR chunks per tile
-// row, RP tile rows per pass of the 256 threads.  Thread t always handles
+// row, RP tile rows per pass of the THREADS threads.  Thread t always handles
 // chunk column t % CPR, rows t / CPR + RP * i.
-template <int BM, int BN>
+template <int BM, int BN, int THREADS>
 struct TileIO {
     static constexpr int CPR = BN / 8;
-    static constexpr int RP = kThreads / CPR;
+    static constexpr int RP = THREADS / CPR;
     static constexpr int PASSES = BM / RP;
     static constexpr int U = PASSES < 8 ? PASSES : 8;
-    static_assert(kThreads % CPR == 0 && BM % RP == 0 && PASSES % U == 0, "tile split");
+    static_assert(THREADS % CPR == 0 && BM % RP == 0 && PASSES % U == 0, "tile split");
 };
 
 // Bytes of the destination resource of one tile (rows_valid x cols_valid,
@@ -137,9 +137,9 @@ __device__ __forceinline__ uint32_t tile_span(int rows_valid, int cols_valid, in
 
 // Copy one finished tile from the local heap to every other heap (the put of
 // Sections 4.1.1 and 4.2.2) and release its counters there.
-template <int BM, int BN, bool NT>
+template <int BM, int BN, int THREADS, bool NT>
 __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
-    using IO = TileIO<BM, BN>;
+    using IO = TileIO<BM, BN, THREADS>;
     const int tid = threadIdx.x;
     const int m0 = tm * BM, n0 = tn * BN;
     const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
@@ -175,28 +175,36 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
 }
 
 // ---------------------------------------------------------------------------
-template <int BM, int BN, bool BF16>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// NW waves per workgroup in a 2 x (NW/2) grid.  With NW = 8 two waves share
+// each SIMD, so one wave's MFMAs run while the other waits on LDS, global
+// loads or the barrier; each wave then holds half the accumulators.
+template <int BM, int BN, bool BF16, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void gas_kernel(const GasParams p) {
-    constexpr int WM = BM / 2, WN = BN / 2;     // wave tile
+    constexpr int THREADS = 64 * NW;
+    constexpr int WGM = 2, WGN = NW / 2;        // wave grid
+    constexpr int WM = BM / WGM, WN = BN / WGN; // wave tile
     constexpr int MI = WM / 32, NI = WN / 32;   // 32x32 MFMA blocks per wave
     constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BN * kRowBytes;
     constexpr int STAGE = A_BYTES + B_BYTES;
     constexpr int C_BYTES = BM * BN * 2;
     constexpr int LDS_BYTES = (2 * STAGE > C_BYTES) ? 2 * STAGE : C_BYTES;
-    constexpr int A_INSTR = BM / 32;            // direct-to-LDS loads per wave per K tile
+    constexpr int A_INSTR = BM / 8 / NW;        // direct-to-LDS loads per wave per K tile
     constexpr int NC = BN / 8;                  // B column chunks
-    constexpr int B_THREADS = NC * (BK / 8);    // threads staging B (8 k rows each)
+    constexpr int B_RU = (NC * (BK / 8) >= THREADS) ? 8 : 4;   // k rows per B staging unit
+    constexpr int B_THREADS = NC * (BK / B_RU); // threads staging B
+    static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     static_assert(MI >= 1 && NI >= 1 && WM % 32 == 0 && WN % 32 == 0, "unsupported tile");
-    static_assert(B_THREADS <= kThreads && B_THREADS % 64 == 0, "B staging split");
-    using IO = TileIO<BM, BN>;
+    static_assert(A_INSTR >= 1 && (BM / 8) % NW == 0, "A staging split");
+    static_assert(B_THREADS <= THREADS && B_THREADS % 64 == 0, "B staging split");
+    using IO = TileIO<BM, BN, THREADS>;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
     __shared__ int s_ok;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WGN, wn = wave % WGN;
     const int pid = blockIdx.x;
 
     // ---------------- consumer workgroups (Section 4.2.2) -----------------
@@ -217,9 +225,9 @@ void gas_kernel(const GasParams p) {
             __syncthreads();
             if (!s_ok) return;
             if (p.nontemporal)
-                put_tile_to_peers<BM, BN, true>(p, tm, tn);
+                put_tile_to_peers<BM, BN, THREADS, true>(p, tm, tn);
             else
-                put_tile_to_peers<BM, BN, false>(p, tm, tn);
+                put_tile_to_peers<BM, BN, THREADS, false>(p, tm, tn);
         }
         return;
     }
@@ -228,17 +236,19 @@ void gas_kernel(const GasParams p) {
     const int G = p.gemm_wgs;
     const int KT = (p.K + BK - 1) / BK;
 
-    // A: wave w, load u fills staged rows 8*(4u+w) .. +7; lane l lands at
-    // LDS position l & 7 of row 8*(4u+w) + (l >> 3), so it fetches the
-    // global chunk that the XOR swizzle maps there.
+    // A: wave w, load u fills staged rows 8*(NW*u + w) .. +7; lane l lands at
+    // LDS position l & 7 of row 8*(NW*u + w) + (l >> 3), so it fetches the
+    // global chunk that the XOR swizzle maps there.  (NW*u + w) & 7 only
+    // depends on the parity of u.
     const int lr = lane >> 3, lc = lane & 7;
-    const int a_chunk_even = lc ^ lr ^ wave;            // u even: (4u + w) & 7 == w
-    const int a_chunk_odd = a_chunk_even ^ 4;           // u odd:  (4u + w) & 7 == w + 4
+    const int a_chunk_even = lc ^ lr ^ (wave & 7);
+    const int a_chunk_odd = lc ^ lr ^ ((NW + wave) & 7);
     const uint32_t a_row_off = (uint32_t)((8 * wave + lr) * p.lda * 2);
-    const uint32_t a_u_bytes = (uint32_t)(32 * p.lda * 2);
-    // B: thread (nc, kg) loads rows 8kg..8kg+7 of column chunk nc.
+    const uint32_t a_u_bytes = (uint32_t)(8 * NW * p.lda * 2);
+    // B: thread (nc, kg) loads rows B_RU*kg .. B_RU*kg + B_RU - 1 of column
+    // chunk nc.
     const int b_nc = tid % NC, b_kg = tid / NC;
-    const uint32_t b_voff = (uint32_t)(b_kg * 8 * p.ldb * 2 + b_nc * 16);
+    const uint32_t b_voff = (uint32_t)(b_kg * B_RU * p.ldb * 2 + b_nc * 16);
     const uint32_t b_row_bytes = (uint32_t)(p.ldb * 2);
 
     for (int t = pid; t < p.num_tiles; t += G) {
@@ -259,7 +269,7 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-        symtile::u32x4 rb[8];
+        symtile::u32x4 rb[B_RU];
 
         // A straight into LDS stage `buf`; B into registers.  Chunks at
         // k >= K read zero (offset outside the resource).
@@ -272,33 +282,44 @@ void gas_kernel(const GasParams p) {
                                        ? a_row_off + a_chunk_odd * 16 : symtile::kOOB;
 #pragma unroll
             for (int u = 0; u < A_INSTR; ++u)
-                symtile::buf_ld16_lds(rA, As + (4 * u + wave) * 1024, (u & 1) ? v_odd : v_even,
-                                      u * a_u_bytes + k0 * 2);
+                symtile::buf_ld16_lds(rA, As + (NW * u + wave) * 1024,
+                                      (u & 1) ? v_odd : v_even, u * a_u_bytes + k0 * 2);
             if (tid < B_THREADS) {
                 const uint32_t kb = (uint32_t)k0 * b_row_bytes;
 #pragma unroll
-                for (int r = 0; r < 8; ++r)
+                for (int r = 0; r < B_RU; ++r)
                     rb[r] = symtile::buf_ld16(rB, b_voff, kb + r * b_row_bytes);
             }
         };
 
-        // B registers -> LDS stage `buf`, transposed 8x8 so each staged row
-        // holds 8 consecutive k of one column.
+        // B registers -> LDS stage `buf`, transposed so each staged row holds
+        // consecutive k of one column (8 rows: whole 16-byte chunks; 4 rows:
+        // the low or high half of a chunk).
         auto stage_b = [&](int buf) {
             if (tid >= B_THREADS) return;
             uint8_t* Bs = smem + buf * STAGE + A_BYTES;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int d = j >> 1;
-                symtile::u32x4 col;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t x = rb[2 * e][d], y = rb[2 * e + 1][d];
-                    col[e] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u)) : ((x & 0xFFFFu) | (y << 16));
-                }
                 const int n = b_nc * 8 + j;
-                *reinterpret_cast<symtile::u32x4*>(Bs + n * kRowBytes + ((b_kg ^ swz(n)) << 4)) =
-                    col;
+                if constexpr (B_RU == 8) {
+                    symtile::u32x4 col;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t x = rb[2 * e][d], y = rb[2 * e + 1][d];
+                        col[e] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u))
+                                         : ((x & 0xFFFFu) | (y << 16));
+                    }
+                    *reinterpret_cast<symtile::u32x4*>(Bs + n * kRowBytes +
+                                                       ((b_kg ^ swz(n)) << 4)) = col;
+                } else {
+                    uint2 col;
+                    const uint32_t x0 = rb[0][d], y0 = rb[1][d], x1 = rb[2][d], y1 = rb[3][d];
+                    col.x = (j & 1) ? ((x0 >> 16) | (y0 & 0xFFFF0000u)) : ((x0 & 0xFFFFu) | (y0 << 16));
+                    col.y = (j & 1) ? ((x1 >> 16) | (y1 & 0xFFFF0000u)) : ((x1 & 0xFFFFu) | (y1 << 16));
+                    *reinterpret_cast<uint2*>(Bs + n * kRowBytes +
+                                              (((b_kg >> 1) ^ swz(n)) << 4) + ((b_kg & 1) << 3)) = col;
+                }
             }
         };
 
@@ -414,7 +435,7 @@ void gas_kernel(const GasParams p) {
                 }
             }
         }
-        symtile::wg_stores_done();
+        symtile::wg_stores_done();     // also orders the LDS reads above before reuse
         if (tid == 0) {
             symtile::release_agent();
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
@@ -431,9 +452,9 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
     for (int t = blockIdx.x; t < p.num_tiles; t += gridDim.x) {
         const int tm = t / p.tiles_n, tn = t % p.tiles_n;
         if (p.nontemporal)
-            put_tile_to_peers<BM, BN, true>(p, tm, tn);
+            put_tile_to_peers<BM, BN, kThreads, true>(p, tm, tn);
         else
-            put_tile_to_peers<BM, BN, false>(p, tm, tn);
+            put_tile_to_peers<BM, BN, kThreads, false>(p, tm, tn);
     }
 }
 
@@ -441,25 +462,31 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
 struct Variant {
     int bm, bn;
     bool bf16;
+    int waves;
     const void* gas;
     const void* scatter;
 };
 
-template <int BM, int BN, bool BF16>
+template <int BM, int BN, bool BF16, int NW>
 Variant make_variant() {
-    return Variant{BM, BN, BF16, reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16>),
+    return Variant{BM, BN, BF16, NW,
+                   reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW>),
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>)};
 }
 
-const Variant* find_variant(int bm, int bn, bool bf16) {
+// waves == 0 picks the first entry of the shape (the default wave count).
+const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
     static const Variant table[] = {
-        make_variant<64, 64, false>(),   make_variant<64, 64, true>(),
-        make_variant<128, 128, false>(), make_variant<128, 128, true>(),
-        make_variant<256, 128, false>(), make_variant<256, 128, true>(),
-        make_variant<256, 256, false>(), make_variant<256, 256, true>(),
+        make_variant<64, 64, false, 4>(),    make_variant<64, 64, true, 4>(),
+        make_variant<128, 128, false, 4>(),  make_variant<128, 128, true, 4>(),
+        make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),
+        make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
+        make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
+        make_variant<256, 128, false, 8>(),  make_variant<256, 128, true, 8>(),
     };
     for (const Variant& v : table)
-        if (v.bm == bm && v.bn == bn && v.bf16 == bf16) return &v;
+        if (v.bm == bm && v.bn == bn && v.bf16 == bf16 && (waves == 0 || v.waves == waves))
+            return &v;
     return nullptr;
 }
 
@@ -467,7 +494,7 @@ symtile_status coresident_limit(const Variant* v, int device, int* cus, int* lim
     int n_cu = symtile_host::cu_count(device);
     if (n_cu <= 0) return symtile_host::fail(SYMTILE_EHIP, "cannot read the CU count");
     int per_cu = 0;
-    SYMTILE_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->gas, kThreads, 0));
+    SYMTILE_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->gas, 64 * v->waves, 0));
     *cus = n_cu;
     *limit = per_cu * n_cu;
     return SYMTILE_OK;
@@ -478,7 +505,7 @@ symtile_status coresident_limit(const Variant* v, int device, int* cus, int* lim
 extern "C" symtile_status symtile_device_info(int device, int tile_m, int tile_n, int* cu_count,
                                               int* max_coresident_wgs) {
     if (tile_m == 0 && tile_n == 0) tile_m = tile_n = 256;
-    const Variant* v = find_variant(tile_m, tile_n, true);
+    const Variant* v = find_variant(tile_m, tile_n, true, 0);
     if (!v) return symtile_host::fail(SYMTILE_EUNSUPPORTED, "tile shape not built");
     int cus = 0, lim = 0;
     if (symtile_status st = coresident_limit(v, device, &cus, &lim)) return st;
@@ -511,8 +538,10 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     if (lda < K || ldb < N_local) return fail(SYMTILE_EINVAL, "lda < K or ldb < N_local");
     if (K % 8 || N_local % 8 || lda % 8 || ldb % 8)
         return fail(SYMTILE_EINVAL, "K, N_local, lda and ldb must be multiples of 8");
-    const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16);
-    if (!v) return fail(SYMTILE_EUNSUPPORTED, "tile shape not built");
+    if (cfg.waves_per_wg != 0 && cfg.waves_per_wg != 4 && cfg.waves_per_wg != 8)
+        return fail(SYMTILE_EINVAL, "waves_per_wg must be 0, 4 or 8");
+    const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16, cfg.waves_per_wg);
+    if (!v) return fail(SYMTILE_EUNSUPPORTED, "tile shape / wave count not built");
     // Buffer resources span one tile row band of A or C and the whole of B;
     // each must stay below 2 GiB.
     const size_t kMaxSpan = size_t(1) << 31;
@@ -591,7 +620,7 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         p.gemm_wgs = g;
         p.role = cfg.variant == SYMTILE_FUSED_SEQ ? ROLE_FUSED : ROLE_LOCAL_ONLY;
         void* args[] = {&p};
-        SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(kThreads), args, 0, stream));
+        SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(64 * v->waves), args, 0, stream));
         if (cfg.variant == SYMTILE_BULK_SYNC && world_size > 1) {
             int c = cfg.copy_wgs > 0 ? cfg.copy_wgs : cus;
             c = std::min(c, ntiles);
@@ -614,6 +643,6 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     p.copy_wgs = c;
     p.role = ROLE_WG_SPEC;
     void* args[] = {&p};
-    SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g + c), dim3(kThreads), args, 0, stream));
+    SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g + c), dim3(64 * v->waves), args, 0, stream));
     return SYMTILE_OK;
 }

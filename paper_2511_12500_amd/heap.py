@@ -132,7 +132,8 @@ class GatheredOutput:
 
     def run(self, A: torch.Tensor, B_shard: torch.Tensor, rank: int, variant: int,
             gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
-            spin_limit: int = 0, epoch: int | None = None, stream: int | None = None) -> None:
+            spin_limit: int = 0, epoch: int | None = None, stream: int | None = None,
+            waves_per_wg: int = 0) -> None:
         """One call of rank ``rank`` (enqueued on the stream, asynchronous).
         For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
         more than after the previous WG_SPEC call on these buffers."""
@@ -148,7 +149,8 @@ class GatheredOutput:
             self.ready_epoch = self.ready_epoch + 1 if epoch is None else epoch
         cfg = B.GasConfig(variant=variant, tile_m=self.tile_m, tile_n=self.tile_n,
                           gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, epoch=max(self.ready_epoch, 1),
-                          spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m)
+                          spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
+                          waves_per_wg=waves_per_wg)
         dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
         B.symtile_gemm_all_scatter(
             self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),

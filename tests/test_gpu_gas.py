@@ -295,3 +295,23 @@ def test_argument_errors():
         call(c0, f0, dtype=pkg.F32)
     assert e.value.name == "EUNSUPPORTED"
     p.heap.barrier()
+
+
+@pytest.mark.parametrize("case", [(8, 1024, 1024, 4096, 256, 256, "bf16"),
+                                  (3, 300, 264, 200, 256, 256, "f16"),
+                                  (2, 512, 256, 320, 256, 128, "bf16")],
+                         ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s" % c)
+def test_four_and_eight_wave_kernels_agree_bitwise(case):
+    """Both wave layouts compute each accumulator in the same order, so the
+    heaps they leave are identical; both match the oracle."""
+    world, M, N, K, tm, tn, dtype = case
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=5)
+    want = {1 % world: oracle_block(p.A, p.shards[1 % world], dtype)}
+    heaps = []
+    for waves in (4, 8):
+        p.sentinel()
+        p.run(1 % world, FUSED, waves_per_wg=waves)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[1 % world]))
+        heaps.append(u16(p.out.C_all()).copy())
+    assert np.array_equal(heaps[0], heaps[1])
