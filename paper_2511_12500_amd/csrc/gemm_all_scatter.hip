@@ -72,6 +72,20 @@ struct GasParams {
     int nontemporal;
 };
 
+// s_waitcnt immediate that waits until at most n LDS (lgkm) operations of
+// this wave are outstanding; vmcnt and expcnt are left at their no-wait
+// maxima (gfx9 encoding: vmcnt 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int lgkm_wait(int n) { return 15 | (3 << 14) | (7 << 4) | ((n & 15) << 8); }
+
+// Wait until at most N LDS reads of this wave are outstanding, with scheduling
+// fences on both sides so no instruction is moved across the wait.
+template <int N>
+__device__ __forceinline__ void wait_lds() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(lgkm_wait(N));
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // XOR swizzle of the 16-byte chunk index inside a 128-byte staged row.
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
 
@@ -353,21 +367,26 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int j = 0; j < NI; ++j) acc[i][j] = mfma32<BF16>(b[j], a[i], acc[i][j]);
         };
+        // LDS reads of substep s+1 are in flight while the MFMAs of substep s
+        // issue: before each MFMA group the wave waits for exactly the older
+        // group of reads (LDS reads complete in order), never for all of them.
+        constexpr int RD = MI + NI;               // LDS reads per substep
         auto compute_tile = [&](int buf) {
             symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
             read_frags(buf, 0, a0, b0);
-            read_frags(buf, 1, a1, b1);
             __builtin_amdgcn_sched_barrier(0);
+            read_frags(buf, 1, a1, b1);
+            wait_lds<RD>();
             mfmas(a0, b0);
             __builtin_amdgcn_sched_barrier(0);
             read_frags(buf, 2, a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
+            wait_lds<RD>();
             mfmas(a1, b1);
             __builtin_amdgcn_sched_barrier(0);
             read_frags(buf, 3, a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
+            wait_lds<RD>();
             mfmas(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
+            wait_lds<0>();
             mfmas(a1, b1);
             __builtin_amdgcn_sched_barrier(0);
         };

@@ -115,43 +115,53 @@ __device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* lds_base, uint32_t 
         r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
 }
 
+// Every pointer in the heap is device (global) memory.  Atomics through a
+// generic pointer compile to flat instructions, which count on both the
+// vector-memory and the LDS counters; while one is outstanding the compiler
+// can only wait for LDS reads with a full drain.  Casting to the global
+// address space keeps LDS waits exact.
+template <typename T>
+__device__ __forceinline__ __attribute__((address_space(1))) T* global_ptr(T* p) {
+    return (__attribute__((address_space(1))) T*)p;
+}
+
 // ---- atomics with ordering and scope (Section 3.3.3) ----------------------
 // SEM is a __ATOMIC_* order, SCOPE a __HIP_MEMORY_SCOPE_* constant.
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_add(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_add(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_add(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_xchg(uint32_t* p, uint32_t v) {
-    return __hip_atomic_exchange(p, v, SEM, SCOPE);
+    return __hip_atomic_exchange(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_cas(uint32_t* p, uint32_t expected, uint32_t desired) {
     // failure order: the strongest of relaxed/acquire not above SEM
     constexpr int FAIL = (SEM == __ATOMIC_ACQUIRE || SEM == __ATOMIC_ACQ_REL) ? __ATOMIC_ACQUIRE
                                                                               : __ATOMIC_RELAXED;
-    __hip_atomic_compare_exchange_strong(p, &expected, desired, SEM, FAIL, SCOPE);
+    __hip_atomic_compare_exchange_strong(global_ptr(p), &expected, desired, SEM, FAIL, SCOPE);
     return expected;   // the value observed
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_and(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_and(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_and(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_or(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_or(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_or(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_xor(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_xor(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_xor(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_min(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_min(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_min(global_ptr(p), v, SEM, SCOPE);
 }
 template <int SEM, int SCOPE>
 __device__ __forceinline__ uint32_t atomic_max(uint32_t* p, uint32_t v) {
-    return __hip_atomic_fetch_max(p, v, SEM, SCOPE);
+    return __hip_atomic_fetch_max(global_ptr(p), v, SEM, SCOPE);
 }
 
 // ---- per-tile flags ------------------------------------------------------
@@ -177,7 +187,7 @@ __device__ __forceinline__ void release_agent() {
 }
 
 __device__ __forceinline__ void flag_add(uint32_t* flag) {
-    __hip_atomic_fetch_add(flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_fetch_add(global_ptr(flag), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Bounded wait by one thread until *flag >= target.  Polls with relaxed
@@ -187,7 +197,7 @@ __device__ __forceinline__ void flag_add(uint32_t* flag) {
 __device__ __forceinline__ bool flag_wait_geq(const uint32_t* flag, uint32_t target,
                                               uint32_t spin_limit) {
     for (uint32_t n = 0; n < spin_limit; ++n) {
-        uint32_t v = __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        uint32_t v = __hip_atomic_load(global_ptr(flag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (v >= target) return true;
         __builtin_amdgcn_s_sleep(1);
     }
@@ -198,7 +208,7 @@ __device__ __forceinline__ bool flag_wait_geq(const uint32_t* flag, uint32_t tar
 enum : uint32_t { ERR_TIMEOUT = 1u };
 
 __device__ __forceinline__ void raise_error(uint32_t* err, uint32_t code) {
-    __hip_atomic_fetch_or(err, code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_fetch_or(global_ptr(err), code, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 }  // namespace symtile
