@@ -17,9 +17,10 @@
 //     accumulators (v_mfma_f32_32x32x16_{bf16,f16}, fp32 accumulate);
 //     A and B tiles of BK = 64 are staged through LDS, double buffered, with
 //     an XOR swizzle that keeps both the staging writes and the fragment
-//     reads free of bank conflicts;  B arrives row-major (N contiguous) and
-//     is transposed 8x8 in registers while staging, so every MFMA operand
-//     is a single 16-byte LDS read of 8 consecutive k;
+//     reads free of bank conflicts.  Both tiles go global -> LDS directly
+//     (buffer loads into LDS), A as [m][k] rows read with 16-byte LDS reads,
+//     B as [k][n] rows, whose MFMA operands (8 consecutive k of one column)
+//     come from two transposing LDS reads (ds_read_b64_tr_b16);
 //   * epilogue (Section 4.2.1): the accumulators are rounded to the output
 //     type (nearest even), restaged through LDS as row-major 16-byte
 //     chunks and written with coalesced 128-bit stores to each destination
@@ -46,6 +47,8 @@ using symtile::u32x4;
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int BK = 64;                 // K depth of one staged tile
@@ -86,8 +89,24 @@ __device__ __forceinline__ void wait_lds() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// XOR swizzle of the 16-byte chunk index inside a 128-byte staged row.
+// s_waitcnt immediate that waits until at most n vector-memory operations
+// of this wave are outstanding (lgkmcnt and expcnt not waited).
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// XOR swizzle of the 16-byte chunk index inside a 128-byte staged A row.
 __device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+
+// XOR swizzle of the 16-byte chunk index inside a staged B row (k fixed,
+// CPR chunks of 8 consecutive n).  A transposing fragment read touches rows
+// k..k+3 and k+8..k+11 (k a multiple of 4) and four adjacent chunks; the
+// swizzle spreads each half-wave's 16 (row, chunk) pairs over distinct
+// 16-byte bank groups.  With 8 chunks per row (128-byte rows) the row parity
+// already selects the bank half, so bit 1 of k takes the place of bit 0.
+template <int CPR>
+__device__ __forceinline__ int swz_b(int k) {
+    const int lo = (CPR >= 16) ? ((k & 3) << 2) : (((k >> 1) & 1) << 2);
+    return lo ^ (((k >> 3) & 1) << 1);
+}
 
 // Producer-order tile index t -> (tile row, tile column).
 __device__ __forceinline__ void tile_coords(int t, int G, const GasParams& p, int& tm, int& tn) {
@@ -199,18 +218,19 @@ void gas_kernel(const GasParams p) {
     constexpr int WGM = 2, WGN = NW / 2;        // wave grid
     constexpr int WM = BM / WGM, WN = BN / WGN; // wave tile
     constexpr int MI = WM / 32, NI = WN / 32;   // 32x32 MFMA blocks per wave
-    constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BN * kRowBytes;
+    constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BK * BN * 2;
     constexpr int STAGE = A_BYTES + B_BYTES;
     constexpr int C_BYTES = BM * BN * 2;
     constexpr int LDS_BYTES = (2 * STAGE > C_BYTES) ? 2 * STAGE : C_BYTES;
     constexpr int A_INSTR = BM / 8 / NW;        // direct-to-LDS loads per wave per K tile
-    constexpr int NC = BN / 8;                  // B column chunks
-    constexpr int B_RU = (NC * (BK / 8) >= THREADS) ? 8 : 4;   // k rows per B staging unit
-    constexpr int B_THREADS = NC * (BK / B_RU); // threads staging B
+    constexpr int ROWB = BN * 2;                // bytes per staged B row (one k)
+    constexpr int CPR = BN / 8;                 // 16-byte chunks per staged B row
+    constexpr int RPI = 1024 / ROWB;            // B rows per 1 KiB direct-to-LDS load
+    constexpr int B_INSTR = BK / RPI / NW;      // direct-to-LDS B loads per wave per K tile
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     static_assert(MI >= 1 && NI >= 1 && WM % 32 == 0 && WN % 32 == 0, "unsupported tile");
     static_assert(A_INSTR >= 1 && (BM / 8) % NW == 0, "A staging split");
-    static_assert(B_THREADS <= THREADS && B_THREADS % 64 == 0, "B staging split");
+    static_assert(RPI >= 1 && B_INSTR >= 1 && (BK / RPI) % NW == 0, "B staging split");
     using IO = TileIO<BM, BN, THREADS>;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
@@ -259,20 +279,32 @@ void gas_kernel(const GasParams p) {
     const int a_chunk_odd = lc ^ lr ^ ((NW + wave) & 7);
     const uint32_t a_row_off = (uint32_t)((8 * wave + lr) * p.lda * 2);
     const uint32_t a_u_bytes = (uint32_t)(8 * NW * p.lda * 2);
-    // B: thread (nc, kg) loads rows B_RU*kg .. B_RU*kg + B_RU - 1 of column
-    // chunk nc.
-    const int b_nc = tid % NC, b_kg = tid / NC;
-    const uint32_t b_voff = (uint32_t)(b_kg * B_RU * p.ldb * 2 + b_nc * 16);
+    // B: wave w, load u fills staged rows RPI*(NW*u + w) .. +RPI-1; lane l
+    // lands at chunk l % CPR of row RPI*(NW*u + w) + l / CPR and fetches the
+    // global chunk the swizzle maps there.  The swizzle reads bits 0, 1 and 3
+    // of the row, so it depends on u only through its parity.
+    const int b_rr = lane / CPR, b_pc = lane % CPR;
+    const int b_k_even = wave * RPI + b_rr, b_k_odd = (NW + wave) * RPI + b_rr;
+    const uint32_t b_row_off = (uint32_t)((wave * RPI + b_rr) * p.ldb * 2);
+    const uint32_t b_v_even = b_row_off + (uint32_t)((b_pc ^ swz_b<CPR>(b_k_even)) * 16);
+    const uint32_t b_v_odd = b_row_off + (uint32_t)((b_pc ^ swz_b<CPR>(b_k_odd)) * 16);
+    const uint32_t b_u_bytes = (uint32_t)(NW * RPI * p.ldb * 2);
     const uint32_t b_row_bytes = (uint32_t)(p.ldb * 2);
+    // Transposing B fragment reads: in each 16-lane group, lane s addresses
+    // row kq + s / 4 and columns 4 * (s % 4) .. +3 of its 16-column half, and
+    // receives 4 consecutive k of column (lane % 32).  kq = 8 * (lane / 32) +
+    // 4 * h (h = 0, 1 for k 0..3 and 4..7 of the operand).
+    const int tr_row = 8 * (lane >> 5) + ((lane & 15) >> 2);
+    const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
     for (int t = pid; t < p.num_tiles; t += G) {
         int tm, tn;
         tile_coords(t, G, p, tm, tn);
         const int m0 = tm * BM, n0 = tn * BN;
         const int rows_a = min(BM, p.M - m0);
-        const symtile::rsrc_t rA =
-            symtile::make_rsrc(p.A + (size_t)m0 * p.lda, (uint32_t)(rows_a * p.lda * 2));
-        const symtile::rsrc_t rB = symtile::make_rsrc(
+        const symtile::i32x4_t rA = symtile::make_rsrc_words(
+            p.A + (size_t)m0 * p.lda, (uint32_t)(rows_a * p.lda * 2));
+        const symtile::i32x4_t rB = symtile::make_rsrc_words(
             p.B + n0, p.K > 0 ? (uint32_t)((size_t)p.K * p.ldb * 2 - (size_t)n0 * 2) : 0u);
 
         f32x16_t acc[MI][NI];
@@ -283,10 +315,9 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-        symtile::u32x4 rb[B_RU];
-
-        // A straight into LDS stage `buf`; B into registers.  Chunks at
-        // k >= K read zero (offset outside the resource).
+        // A and B straight into LDS stage `buf`.  A chunks at k >= K read
+        // zero (offset replaced by one outside the resource); B rows at
+        // k >= K lie past the end of B's resource and read zero too.
         auto load_tile = [&](int kt, int buf) {
             const int k0 = kt * BK;
             uint8_t* As = smem + buf * STAGE;
@@ -296,45 +327,14 @@ void gas_kernel(const GasParams p) {
                                        ? a_row_off + a_chunk_odd * 16 : symtile::kOOB;
 #pragma unroll
             for (int u = 0; u < A_INSTR; ++u)
-                symtile::buf_ld16_lds(rA, As + (NW * u + wave) * 1024,
-                                      (u & 1) ? v_odd : v_even, u * a_u_bytes + k0 * 2);
-            if (tid < B_THREADS) {
-                const uint32_t kb = (uint32_t)k0 * b_row_bytes;
+                symtile::buf_ld16_lds_async(rA, symtile::lds_addr(As + (NW * u + wave) * 1024),
+                                            (u & 1) ? v_odd : v_even, u * a_u_bytes + k0 * 2);
+            uint8_t* Bs = As + A_BYTES;
+            const uint32_t kb = (uint32_t)k0 * b_row_bytes;
 #pragma unroll
-                for (int r = 0; r < B_RU; ++r)
-                    rb[r] = symtile::buf_ld16(rB, b_voff, kb + r * b_row_bytes);
-            }
-        };
-
-        // B registers -> LDS stage `buf`, transposed so each staged row holds
-        // consecutive k of one column (8 rows: whole 16-byte chunks; 4 rows:
-        // the low or high half of a chunk).
-        auto stage_b = [&](int buf) {
-            if (tid >= B_THREADS) return;
-            uint8_t* Bs = smem + buf * STAGE + A_BYTES;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int d = j >> 1;
-                const int n = b_nc * 8 + j;
-                if constexpr (B_RU == 8) {
-                    symtile::u32x4 col;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t x = rb[2 * e][d], y = rb[2 * e + 1][d];
-                        col[e] = (j & 1) ? ((x >> 16) | (y & 0xFFFF0000u))
-                                         : ((x & 0xFFFFu) | (y << 16));
-                    }
-                    *reinterpret_cast<symtile::u32x4*>(Bs + n * kRowBytes +
-                                                       ((b_kg ^ swz(n)) << 4)) = col;
-                } else {
-                    uint2 col;
-                    const uint32_t x0 = rb[0][d], y0 = rb[1][d], x1 = rb[2][d], y1 = rb[3][d];
-                    col.x = (j & 1) ? ((x0 >> 16) | (y0 & 0xFFFF0000u)) : ((x0 & 0xFFFFu) | (y0 << 16));
-                    col.y = (j & 1) ? ((x1 >> 16) | (y1 & 0xFFFF0000u)) : ((x1 & 0xFFFFu) | (y1 << 16));
-                    *reinterpret_cast<uint2*>(Bs + n * kRowBytes +
-                                              (((b_kg >> 1) ^ swz(n)) << 4) + ((b_kg & 1) << 3)) = col;
-                }
-            }
+            for (int u = 0; u < B_INSTR; ++u)
+                symtile::buf_ld16_lds_async(rB, symtile::lds_addr(Bs + (NW * u + wave) * 1024),
+                                            (u & 1) ? b_v_odd : b_v_even, u * b_u_bytes + kb);
         };
 
         // MFMAs over LDS stage `buf`.  Operands are swapped (B fragment as
@@ -356,9 +356,18 @@ void gas_kernel(const GasParams p) {
             }
 #pragma unroll
             for (int j = 0; j < NI; ++j) {
-                const int row = wn * WN + j * 32 + (lane & 31);
-                b[j] = *reinterpret_cast<const symtile::u32x4*>(Bs + row * kRowBytes +
-                                                               ((c ^ swz(row)) << 4));
+                const int col = wn * WN + j * 32 + tr_col;
+                u32x2_t h[2];
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {
+                    const int k = 16 * s + tr_row + 4 * half;
+                    const uint8_t* q = Bs + k * ROWB + ((((col >> 3) ^ swz_b<CPR>(k))) << 4) +
+                                       ((col & 4) << 1);
+                    h[half] = __builtin_bit_cast(
+                        u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                     (__attribute__((address_space(3))) s16x4_t*)(q)));
+                }
+                b[j] = symtile::u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
             }
         };
         auto mfmas = [&](const symtile::u32x4 (&a)[MI], const symtile::u32x4 (&b)[NI]) {
@@ -370,7 +379,7 @@ void gas_kernel(const GasParams p) {
         // LDS reads of substep s+1 are in flight while the MFMAs of substep s
         // issue: before each MFMA group the wave waits for exactly the older
         // group of reads (LDS reads complete in order), never for all of them.
-        constexpr int RD = MI + NI;               // LDS reads per substep
+        constexpr int RD = MI + 2 * NI;           // LDS reads per substep
         auto compute_tile = [&](int buf) {
             symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
             read_frags(buf, 0, a0, b0);
@@ -391,16 +400,18 @@ void gas_kernel(const GasParams p) {
             __builtin_amdgcn_sched_barrier(0);
         };
 
+        // Each wave waits for its own loads into LDS (vmcnt), then the
+        // barrier makes every wave's loads visible to all.
         if (KT > 0) {
             load_tile(0, 0);
-            stage_b(0);
+            __builtin_amdgcn_s_waitcnt(vm_wait(0));
             __syncthreads();
         }
         for (int kt = 0; kt < KT; ++kt) {
             const int cur = kt & 1;
             if (kt + 1 < KT) load_tile(kt + 1, cur ^ 1);
             compute_tile(cur);
-            if (kt + 1 < KT) stage_b(cur ^ 1);
+            __builtin_amdgcn_s_waitcnt(vm_wait(0));
             __syncthreads();
         }
 

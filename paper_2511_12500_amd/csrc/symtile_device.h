@@ -107,6 +107,40 @@ __device__ __forceinline__ void buf_st16(u32x4 v, rsrc_t r, uint32_t voff, uint3
     buf_st16p<NT ? kStoreNonTemporal : kStoreDefault>(v, r, voff, soff);
 }
 
+// Descriptor words of the same buffer resource, for inline assembly.
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4_t make_rsrc_words(const void* base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    return i32x4_t{(int)__builtin_amdgcn_readfirstlane((uint32_t)b),
+                   (int)(__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) & 0xFFFFu),
+                   (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000};
+}
+
+// 16 bytes per lane from the buffer straight into LDS (lane l writes
+// lds_addr + 16 * l), issued from inline assembly so that the compiler does
+// not track it.  The compiler cannot tell which LDS bytes a direct-to-LDS
+// load writes, so for a tracked one it drains every such load before any
+// later LDS read, including reads of other pipeline stages; with this form
+// the caller orders the load itself: s_waitcnt vmcnt, then a barrier, before
+// any wave reads the bytes.  M0 carries the LDS address (one wait state
+// between writing M0 and the load).
+__device__ __forceinline__ void buf_ld16_lds_async(const i32x4_t& r, uint32_t lds_addr,
+                                                   uint32_t voff, uint32_t soff) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, %3 offen lds"
+        :
+        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(r),
+          "s"(__builtin_amdgcn_readfirstlane(soff))
+        : "memory", "m0");
+}
+
+// LDS byte address of a pointer into __shared__ memory.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
 // 16 bytes per lane from the buffer straight into LDS: lane l of the wave
 // writes lds_base + 16 * l (lds_base is wave-uniform).
 __device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* lds_base, uint32_t voff,
