@@ -51,8 +51,10 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int BK = 64;                 // K depth of one staged tile
-constexpr int kRowBytes = BK * 2;      // LDS bytes per staged row (8 chunks of 16 B)
+constexpr int BK = 32;                 // K depth of one pipeline stage
+constexpr int kRowBytes = BK * 2;      // LDS bytes per staged A row (4 chunks of 16 B)
+constexpr int NS = 4;                  // pipeline stages (LDS ring)
+constexpr int PD = 3;                  // prefetch distance in stages (< NS)
 
 enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2 };
 
@@ -93,8 +95,21 @@ __device__ __forceinline__ void wait_lds() {
 // of this wave are outstanding (lgkmcnt and expcnt not waited).
 constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
-// XOR swizzle of the 16-byte chunk index inside a 128-byte staged A row.
-__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+// Workgroup barrier for the LDS hand-off inside the pipelined loop.  The
+// caller has already waited for its own LDS reads (lgkmcnt) and its loads
+// into LDS (vmcnt); unlike __syncthreads() this adds no wait for the loads
+// still in flight for later stages.  The empty asm statements keep the
+// compiler from moving memory accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// XOR swizzle of the 16-byte chunk index inside a 64-byte staged A row.  A
+// fragment read has 16 consecutive rows per 256-byte bank window: the row's
+// bits 0-1 pick the 64-byte quarter, bits 2-3 permute the chunk within it.
+__device__ __forceinline__ int swz(int row) { return (row >> 2) & 3; }
 
 // XOR swizzle of the 16-byte chunk index inside a staged B row (k fixed,
 // CPR chunks of 8 consecutive n).  A transposing fragment read touches rows
@@ -221,15 +236,16 @@ void gas_kernel(const GasParams p) {
     constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BK * BN * 2;
     constexpr int STAGE = A_BYTES + B_BYTES;
     constexpr int C_BYTES = BM * BN * 2;
-    constexpr int LDS_BYTES = (2 * STAGE > C_BYTES) ? 2 * STAGE : C_BYTES;
-    constexpr int A_INSTR = BM / 8 / NW;        // direct-to-LDS loads per wave per K tile
+    constexpr int LDS_BYTES = (NS * STAGE > C_BYTES) ? NS * STAGE : C_BYTES;
+    constexpr int A_RPI = 1024 / kRowBytes;     // A rows per 1 KiB direct-to-LDS load
+    constexpr int A_INSTR = BM / A_RPI / NW;    // direct-to-LDS A loads per wave per stage
     constexpr int ROWB = BN * 2;                // bytes per staged B row (one k)
     constexpr int CPR = BN / 8;                 // 16-byte chunks per staged B row
     constexpr int RPI = 1024 / ROWB;            // B rows per 1 KiB direct-to-LDS load
-    constexpr int B_INSTR = BK / RPI / NW;      // direct-to-LDS B loads per wave per K tile
+    constexpr int B_INSTR = BK / RPI / NW;      // direct-to-LDS B loads per wave per stage
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     static_assert(MI >= 1 && NI >= 1 && WM % 32 == 0 && WN % 32 == 0, "unsupported tile");
-    static_assert(A_INSTR >= 1 && (BM / 8) % NW == 0, "A staging split");
+    static_assert(A_INSTR >= 1 && (BM / A_RPI) % NW == 0, "A staging split");
     static_assert(RPI >= 1 && B_INSTR >= 1 && (BK / RPI) % NW == 0, "B staging split");
     using IO = TileIO<BM, BN, THREADS>;
 
@@ -270,15 +286,14 @@ void gas_kernel(const GasParams p) {
     const int G = p.gemm_wgs;
     const int KT = (p.K + BK - 1) / BK;
 
-    // A: wave w, load u fills staged rows 8*(NW*u + w) .. +7; lane l lands at
-    // LDS position l & 7 of row 8*(NW*u + w) + (l >> 3), so it fetches the
-    // global chunk that the XOR swizzle maps there.  (NW*u + w) & 7 only
-    // depends on the parity of u.
-    const int lr = lane >> 3, lc = lane & 7;
-    const int a_chunk_even = lc ^ lr ^ (wave & 7);
-    const int a_chunk_odd = lc ^ lr ^ ((NW + wave) & 7);
-    const uint32_t a_row_off = (uint32_t)((8 * wave + lr) * p.lda * 2);
-    const uint32_t a_u_bytes = (uint32_t)(8 * NW * p.lda * 2);
+    // A: wave w, load u fills staged rows A_RPI*(NW*u + w) .. +A_RPI-1; lane
+    // l lands at chunk l % 4 of row A_RPI*(NW*u + w) + l / 4 and fetches the
+    // global chunk the swizzle maps there (the swizzle reads row bits 2-3,
+    // which only depend on the lane).
+    const int a_rr = lane >> 2;
+    const int a_chunk = (lane & 3) ^ swz(a_rr);
+    const uint32_t a_row_off = (uint32_t)((A_RPI * wave + a_rr) * p.lda * 2);
+    const uint32_t a_u_bytes = (uint32_t)(A_RPI * NW * p.lda * 2);
     // B: wave w, load u fills staged rows RPI*(NW*u + w) .. +RPI-1; lane l
     // lands at chunk l % CPR of row RPI*(NW*u + w) + l / CPR and fetches the
     // global chunk the swizzle maps there.  The swizzle reads bits 0, 1 and 3
@@ -321,14 +336,12 @@ void gas_kernel(const GasParams p) {
         auto load_tile = [&](int kt, int buf) {
             const int k0 = kt * BK;
             uint8_t* As = smem + buf * STAGE;
-            const uint32_t v_even = (k0 + 8 * a_chunk_even < p.K)
-                                        ? a_row_off + a_chunk_even * 16 : symtile::kOOB;
-            const uint32_t v_odd = (k0 + 8 * a_chunk_odd < p.K)
-                                       ? a_row_off + a_chunk_odd * 16 : symtile::kOOB;
+            const uint32_t va = (k0 + 8 * a_chunk < p.K) ? a_row_off + a_chunk * 16
+                                                          : symtile::kOOB;
 #pragma unroll
             for (int u = 0; u < A_INSTR; ++u)
                 symtile::buf_ld16_lds_async(rA, symtile::lds_addr(As + (NW * u + wave) * 1024),
-                                            (u & 1) ? v_odd : v_even, u * a_u_bytes + k0 * 2);
+                                            va, u * a_u_bytes + k0 * 2);
             uint8_t* Bs = As + A_BYTES;
             const uint32_t kb = (uint32_t)k0 * b_row_bytes;
 #pragma unroll
@@ -376,44 +389,56 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int j = 0; j < NI; ++j) acc[i][j] = mfma32<BF16>(b[j], a[i], acc[i][j]);
         };
-        // LDS reads of substep s+1 are in flight while the MFMAs of substep s
-        // issue: before each MFMA group the wave waits for exactly the older
-        // group of reads (LDS reads complete in order), never for all of them.
+        // Pipeline over an LDS ring of NS stages of BK = 32 (two k16
+        // substeps each), loads issued PD stages ahead.  Stage kt is read
+        // into fragment set 0 (substep 0) and set 1 (substep 1).  The loop is
+        // rotated so that the MFMAs of stage kt-1's substep 1 issue right
+        // after the barrier, while the reads of stage kt's substep 0 are in
+        // flight: no wave waits on LDS after a barrier.  Before each MFMA
+        // group a wave waits for exactly the older group of reads (LDS reads
+        // complete in order).  Loads into LDS are not tracked by the
+        // compiler: each wave waits for its own with vmcnt, leaving the later
+        // stages' loads in flight, and the barrier then publishes the stage.
         constexpr int RD = MI + 2 * NI;           // LDS reads per substep
-        auto compute_tile = [&](int buf) {
-            symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
+        constexpr int LPS = A_INSTR + B_INSTR;    // loads per wave per stage
+        static_assert((PD - 1) * LPS <= 63 && NS > PD, "pipeline depth");
+        symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
+#pragma unroll
+        for (int i = 0; i < MI; ++i) a1[i] = symtile::u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < NI; ++j) b1[j] = symtile::u32x4{0u, 0u, 0u, 0u};
+
+#pragma unroll
+        for (int d = 0; d < PD; ++d)
+            if (d < KT) load_tile(d, d);
+        for (int kt = 0; kt < KT; ++kt) {
+            const int buf = kt % NS;
+            // this wave's loads of stage kt are done; those of the stages
+            // after it (at most PD-1 of them) may still be in flight
+            if (kt + 2 < KT) {
+                __builtin_amdgcn_s_waitcnt(vm_wait((PD - 1) * LPS));
+            } else if (kt + 1 < KT) {
+                __builtin_amdgcn_s_waitcnt(vm_wait(LPS));
+            } else {
+                __builtin_amdgcn_s_waitcnt(vm_wait(0));
+            }
+            wait_lds<0>();         // stage kt-1's last fragments are in registers
+            ring_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            // every wave is past stage kt-1: its slot takes stage kt+PD
+            if (kt + PD < KT) load_tile(kt + PD, (kt + PD) % NS);
             read_frags(buf, 0, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(a1, b1);         // stage kt-1, substep 1 (zeros when kt = 0)
             __builtin_amdgcn_sched_barrier(0);
             read_frags(buf, 1, a1, b1);
             wait_lds<RD>();
             mfmas(a0, b0);
             __builtin_amdgcn_sched_barrier(0);
-            read_frags(buf, 2, a0, b0);
-            wait_lds<RD>();
-            mfmas(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            read_frags(buf, 3, a1, b1);
-            wait_lds<RD>();
-            mfmas(a0, b0);
-            wait_lds<0>();
-            mfmas(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-        };
-
-        // Each wave waits for its own loads into LDS (vmcnt), then the
-        // barrier makes every wave's loads visible to all.
-        if (KT > 0) {
-            load_tile(0, 0);
-            __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            __syncthreads();
         }
-        for (int kt = 0; kt < KT; ++kt) {
-            const int cur = kt & 1;
-            if (kt + 1 < KT) load_tile(kt + 1, cur ^ 1);
-            compute_tile(cur);
-            __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            __syncthreads();
-        }
+        wait_lds<0>();
+        mfmas(a1, b1);             // last stage, substep 1
+        __syncthreads();           // every wave is done with the ring
 
         // ---- epilogue: round, restage row-major, store, release --------
         uint8_t* Cs = smem;
