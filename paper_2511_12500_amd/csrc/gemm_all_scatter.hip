@@ -36,6 +36,7 @@
 
 #include <algorithm>
 #include <string>
+#include <type_traits>
 
 #include "symtile.h"
 #include "symtile_device.h"
@@ -47,6 +48,7 @@ using symtile::u32x4;
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
@@ -150,6 +152,16 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4 a, u32x4 b, f32x16_t c) {
                                                       __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
 }
 
+template <bool BF16>
+__device__ __forceinline__ f32x4_t mfma16(u32x4 a, u32x4 b, f32x4_t c) {
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
+                                                      __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+
 // Round two fp32 values to the 16-bit output type (nearest even) and pack.
 template <bool BF16>
 __device__ __forceinline__ uint32_t cvt_pack(float x, float y) {
@@ -165,12 +177,16 @@ __device__ __forceinline__ uint32_t cvt_pack(float x, float y) {
 }
 
 // ---------------------------------------------------------------------------
-// Geometry of one output tile for 16-byte row chunks: CPR chunks per tile
-// row, RP tile rows per pass of the THREADS threads.  Thread t always handles
-// chunk column t % CPR, rows t / CPR + RP * i.
+// Tile widths are staged and moved as BN rounded up to a power of two (64,
+// 128 or 256 columns); chunks past the tile's columns are masked.
+constexpr int staged_width(int bn) { return bn <= 64 ? 64 : bn <= 128 ? 128 : 256; }
+
+// Geometry of one output tile for 16-byte row chunks: CPR chunks per staged
+// tile row, RP tile rows per pass of the THREADS threads.  Thread t always
+// handles chunk column t % CPR, rows t / CPR + RP * i.
 template <int BM, int BN, int THREADS>
 struct TileIO {
-    static constexpr int CPR = BN / 8;
+    static constexpr int CPR = staged_width(BN) / 8;
     static constexpr int RP = THREADS / CPR;
     static constexpr int PASSES = BM / RP;
     static constexpr int U = PASSES < 8 ? PASSES : 8;
@@ -223,31 +239,42 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
 }
 
 // ---------------------------------------------------------------------------
-// NW waves per workgroup in a 2 x (NW/2) grid.  With NW = 8 two waves share
-// each SIMD, so one wave's MFMAs run while the other waits on LDS, global
-// loads or the barrier; each wave then holds half the accumulators.
-template <int BM, int BN, bool BF16, int NW>
+// Producer tile shapes.  MF = 32: v_mfma_f32_32x32x16, waves in a 2 x (NW/2)
+// grid, each stage read as two k16 substeps.  MF = 16: v_mfma_f32_16x16x32
+// (same rate per flop), waves in a 4 x (NW/4) grid, one k32 substep per
+// stage; it allows tile widths that are a multiple of 16 but not of 64 (a
+// 256 x 224 tile covers N = 3584 in 16 columns).  B is staged BNS = BN
+// rounded up to a power of two wide, so direct-to-LDS loads stay whole rows;
+// staged columns past BN are loaded but never read.  With NW = 8 two waves
+// share each SIMD, so one wave's MFMAs run while the other waits on LDS,
+// global loads or the barrier.
+template <int BM, int BN, bool BF16, int NW, int MF>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void gas_kernel(const GasParams p) {
     constexpr int THREADS = 64 * NW;
-    constexpr int WGM = 2, WGN = NW / 2;        // wave grid
-    constexpr int WM = BM / WGM, WN = BN / WGN; // wave tile
-    constexpr int MI = WM / 32, NI = WN / 32;   // 32x32 MFMA blocks per wave
-    constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BK * BN * 2;
+    constexpr int WGM = (MF == 32) ? 2 : 4, WGN = NW / WGM;   // wave grid
+    constexpr int WM = BM / WGM, WN = BN / WGN;               // wave tile
+    constexpr int MI = WM / MF, NI = WN / MF;                 // MFMA blocks per wave
+    constexpr int BNS = staged_width(BN);
+    constexpr int A_BYTES = BM * kRowBytes, B_BYTES = BK * BNS * 2;
     constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int C_BYTES = BM * BN * 2;
+    constexpr int CROW = BNS * 2;                             // bytes per staged C row
+    constexpr int C_BYTES = BM * CROW;
     constexpr int LDS_BYTES = (NS * STAGE > C_BYTES) ? NS * STAGE : C_BYTES;
     constexpr int A_RPI = 1024 / kRowBytes;     // A rows per 1 KiB direct-to-LDS load
     constexpr int A_INSTR = BM / A_RPI / NW;    // direct-to-LDS A loads per wave per stage
-    constexpr int ROWB = BN * 2;                // bytes per staged B row (one k)
-    constexpr int CPR = BN / 8;                 // 16-byte chunks per staged B row
+    constexpr int ROWB = BNS * 2;               // bytes per staged B row (one k)
+    constexpr int CPR = BNS / 8;                // 16-byte chunks per staged B row
     constexpr int RPI = 1024 / ROWB;            // B rows per 1 KiB direct-to-LDS load
     constexpr int B_INSTR = BK / RPI / NW;      // direct-to-LDS B loads per wave per stage
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
-    static_assert(MI >= 1 && NI >= 1 && WM % 32 == 0 && WN % 32 == 0, "unsupported tile");
+    static_assert(MF == 32 || MF == 16, "MFMA shape");
+    static_assert(MI >= 1 && NI >= 1 && WM % MF == 0 && WN % MF == 0, "unsupported tile");
     static_assert(A_INSTR >= 1 && (BM / A_RPI) % NW == 0, "A staging split");
     static_assert(RPI >= 1 && B_INSTR >= 1 && (BK / RPI) % NW == 0, "B staging split");
     using IO = TileIO<BM, BN, THREADS>;
+    using acc_t = std::conditional_t<MF == 32, f32x16_t, f32x4_t>;
+    constexpr int ACC_N = (MF == 32) ? 16 : 4;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
     __shared__ int s_ok;
@@ -305,12 +332,14 @@ void gas_kernel(const GasParams p) {
     const uint32_t b_v_odd = b_row_off + (uint32_t)((b_pc ^ swz_b<CPR>(b_k_odd)) * 16);
     const uint32_t b_u_bytes = (uint32_t)(NW * RPI * p.ldb * 2);
     const uint32_t b_row_bytes = (uint32_t)(p.ldb * 2);
-    // Transposing B fragment reads: in each 16-lane group, lane s addresses
-    // row kq + s / 4 and columns 4 * (s % 4) .. +3 of its 16-column half, and
-    // receives 4 consecutive k of column (lane % 32).  kq = 8 * (lane / 32) +
-    // 4 * h (h = 0, 1 for k 0..3 and 4..7 of the operand).
-    const int tr_row = 8 * (lane >> 5) + ((lane & 15) >> 2);
-    const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    // Fragment reads.  A operand (second MFMA source): lane l holds 8
+    // consecutive k of row (l % MF).  B operand (first source) from two
+    // transposing reads: in each 16-lane group, lane s addresses row
+    // kq + s / 4 and columns 4 * (s % 4) .. +3 of a 16-column block, and
+    // receives 4 consecutive k of column (s of that block).
+    const int a_row_lane = lane % MF;
+    const int tr_row = ((MF == 32) ? 8 * (lane >> 5) : 8 * (lane >> 4)) + ((lane & 15) >> 2);
+    const int tr_col = ((MF == 32) ? 16 * ((lane >> 4) & 1) : 0) + 4 * (lane & 3);
 
     for (int t = pid; t < p.num_tiles; t += G) {
         int tm, tn;
@@ -322,13 +351,13 @@ void gas_kernel(const GasParams p) {
         const symtile::i32x4_t rB = symtile::make_rsrc_words(
             p.B + n0, p.K > 0 ? (uint32_t)((size_t)p.K * p.ldb * 2 - (size_t)n0 * 2) : 0u);
 
-        f32x16_t acc[MI][NI];
+        acc_t acc[MI][NI];
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+                for (int e = 0; e < ACC_N; ++e) acc[i][j][e] = 0.0f;
 
         // A and B straight into LDS stage `buf`.  A chunks at k >= K read
         // zero (offset replaced by one outside the resource); B rows at
@@ -350,69 +379,52 @@ void gas_kernel(const GasParams p) {
                                             (u & 1) ? b_v_odd : b_v_even, u * b_u_bytes + kb);
         };
 
-        // MFMAs over LDS stage `buf`.  Operands are swapped (B fragment as
-        // the first source) so each lane's accumulators hold 4 consecutive
-        // columns of one row of C, which makes the epilogue restage cheap.
-        // Fragments are double buffered across the four k16 substeps: the
-        // LDS reads of substep s+1 are issued before the MFMAs of substep s,
-        // and scheduling fences keep the compiler from hoisting further
-        // (which would raise register pressure past the budget).
-        auto read_frags = [&](int buf, int s, symtile::u32x4 (&a)[MI], symtile::u32x4 (&b)[NI]) {
+        // Fragment of A block i (rows wm*WM + i*MF ..) at 16-byte chunk c,
+        // and of B block j (columns wn*WN + j*MF ..) at k offset kbase.
+        auto read_a = [&](int buf, int i, int c) {
             const uint8_t* As = smem + buf * STAGE;
-            const uint8_t* Bs = As + A_BYTES;
-            const int c = 2 * s + (lane >> 5);
-#pragma unroll
-            for (int i = 0; i < MI; ++i) {
-                const int row = wm * WM + i * 32 + (lane & 31);
-                a[i] = *reinterpret_cast<const symtile::u32x4*>(As + row * kRowBytes +
-                                                               ((c ^ swz(row)) << 4));
-            }
-#pragma unroll
-            for (int j = 0; j < NI; ++j) {
-                const int col = wn * WN + j * 32 + tr_col;
-                u32x2_t h[2];
-#pragma unroll
-                for (int half = 0; half < 2; ++half) {
-                    const int k = 16 * s + tr_row + 4 * half;
-                    const uint8_t* q = Bs + k * ROWB + ((((col >> 3) ^ swz_b<CPR>(k))) << 4) +
-                                       ((col & 4) << 1);
-                    h[half] = __builtin_bit_cast(
-                        u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                     (__attribute__((address_space(3))) s16x4_t*)(q)));
-                }
-                b[j] = symtile::u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
-            }
+            const int row = wm * WM + i * MF + a_row_lane;
+            return *reinterpret_cast<const symtile::u32x4*>(As + row * kRowBytes +
+                                                           ((c ^ swz(row)) << 4));
         };
-        auto mfmas = [&](const symtile::u32x4 (&a)[MI], const symtile::u32x4 (&b)[NI]) {
+        auto read_b = [&](int buf, int j, int kbase) {
+            const uint8_t* Bs = smem + buf * STAGE + A_BYTES;
+            const int col = wn * WN + j * MF + tr_col;
+            u32x2_t h[2];
 #pragma unroll
-            for (int i = 0; i < MI; ++i)
-#pragma unroll
-                for (int j = 0; j < NI; ++j) acc[i][j] = mfma32<BF16>(b[j], a[i], acc[i][j]);
+            for (int half = 0; half < 2; ++half) {
+                const int k = kbase + tr_row + 4 * half;
+                const uint8_t* q = Bs + k * ROWB + (((col >> 3) ^ swz_b<CPR>(k)) << 4) +
+                                   ((col & 4) << 1);
+                h[half] = __builtin_bit_cast(
+                    u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                 (__attribute__((address_space(3))) s16x4_t*)(q)));
+            }
+            return symtile::u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
         };
-        // Pipeline over an LDS ring of NS stages of BK = 32 (two k16
-        // substeps each), loads issued PD stages ahead.  Stage kt is read
-        // into fragment set 0 (substep 0) and set 1 (substep 1).  The loop is
-        // rotated so that the MFMAs of stage kt-1's substep 1 issue right
-        // after the barrier, while the reads of stage kt's substep 0 are in
-        // flight: no wave waits on LDS after a barrier.  Before each MFMA
-        // group a wave waits for exactly the older group of reads (LDS reads
-        // complete in order).  Loads into LDS are not tracked by the
-        // compiler: each wave waits for its own with vmcnt, leaving the later
-        // stages' loads in flight, and the barrier then publishes the stage.
-        constexpr int RD = MI + 2 * NI;           // LDS reads per substep
+        // Operands are swapped (B fragment as the first source) so each
+        // lane's accumulators hold 4 consecutive columns of one row of C,
+        // which makes the epilogue restage cheap.
+        auto mma = [&](int i, int j, const symtile::u32x4& a, const symtile::u32x4& b) {
+            if constexpr (MF == 32)
+                acc[i][j] = mfma32<BF16>(b, a, acc[i][j]);
+            else
+                acc[i][j] = mfma16<BF16>(b, a, acc[i][j]);
+        };
+
+        // Pipeline over an LDS ring of NS stages of BK = 32, loads issued PD
+        // stages ahead.  Each stage's fragment reads form two groups; the
+        // loop is rotated so that the MFMAs of stage kt-1's second group
+        // issue right after the barrier, while the reads of stage kt's first
+        // group are in flight: no wave waits on LDS after a barrier.  Before
+        // each MFMA group a wave waits for exactly the older group of reads
+        // (LDS reads complete in order).  Loads into LDS are not tracked by
+        // the compiler: each wave waits for its own with vmcnt, leaving the
+        // later stages' loads in flight, and the barrier then publishes the
+        // stage.
         constexpr int LPS = A_INSTR + B_INSTR;    // loads per wave per stage
         static_assert((PD - 1) * LPS <= 63 && NS > PD, "pipeline depth");
-        symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
-#pragma unroll
-        for (int i = 0; i < MI; ++i) a1[i] = symtile::u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < NI; ++j) b1[j] = symtile::u32x4{0u, 0u, 0u, 0u};
-
-#pragma unroll
-        for (int d = 0; d < PD; ++d)
-            if (d < KT) load_tile(d, d);
-        for (int kt = 0; kt < KT; ++kt) {
-            const int buf = kt % NS;
+        auto stage_ready = [&](int kt) {
             // this wave's loads of stage kt are done; those of the stages
             // after it (at most PD-1 of them) may still be in flight
             if (kt + 2 < KT) {
@@ -422,35 +434,109 @@ void gas_kernel(const GasParams p) {
             } else {
                 __builtin_amdgcn_s_waitcnt(vm_wait(0));
             }
-            wait_lds<0>();         // stage kt-1's last fragments are in registers
+            wait_lds<0>();         // the previous stage's last fragments are in registers
             ring_barrier();
             __builtin_amdgcn_sched_barrier(0);
             // every wave is past stage kt-1: its slot takes stage kt+PD
             if (kt + PD < KT) load_tile(kt + PD, (kt + PD) % NS);
-            read_frags(buf, 0, a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(a1, b1);         // stage kt-1, substep 1 (zeros when kt = 0)
-            __builtin_amdgcn_sched_barrier(0);
-            read_frags(buf, 1, a1, b1);
-            wait_lds<RD>();
-            mfmas(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
+        };
+
+#pragma unroll
+        for (int d = 0; d < PD; ++d)
+            if (d < KT) load_tile(d, d);
+
+        if constexpr (MF == 32) {
+            // group 0 = k16 substep 0 (A and B), group 1 = substep 1.
+            constexpr int RD = MI + 2 * NI;       // LDS reads per group
+            symtile::u32x4 a0[MI], b0[NI], a1[MI], b1[NI];
+#pragma unroll
+            for (int i = 0; i < MI; ++i) a1[i] = symtile::u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < NI; ++j) b1[j] = symtile::u32x4{0u, 0u, 0u, 0u};
+            auto read_group = [&](int buf, int s, symtile::u32x4 (&a)[MI], symtile::u32x4 (&b)[NI]) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i) a[i] = read_a(buf, i, 2 * s + (lane >> 5));
+#pragma unroll
+                for (int j = 0; j < NI; ++j) b[j] = read_b(buf, j, 16 * s);
+            };
+            auto mfmas = [&](const symtile::u32x4 (&a)[MI], const symtile::u32x4 (&b)[NI]) {
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j) mma(i, j, a[i], b[j]);
+            };
+            for (int kt = 0; kt < KT; ++kt) {
+                const int buf = kt % NS;
+                stage_ready(kt);
+                read_group(buf, 0, a0, b0);
+                __builtin_amdgcn_sched_barrier(0);
+                mfmas(a1, b1);     // stage kt-1, substep 1 (zeros when kt = 0)
+                __builtin_amdgcn_sched_barrier(0);
+                read_group(buf, 1, a1, b1);
+                wait_lds<RD>();
+                mfmas(a0, b0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            wait_lds<0>();
+            mfmas(a1, b1);         // last stage, substep 1
+        } else {
+            // One k32 substep per stage.  Group 0 = the A fragments and B
+            // blocks [0, NJ0); group 1 = B blocks [NJ0, NI).  The MFMAs of
+            // group 1 need the A fragments of their own stage, kept in aprev
+            // while the next stage's A fragments are read.
+            constexpr int NJ0 = (NI + 1) / 2, NJ1 = NI - NJ0;
+            constexpr int RD1 = 2 * NJ1;          // LDS reads of group 1
+            symtile::u32x4 acur[MI], aprev[MI], b0[NJ0], b1[NJ1 > 0 ? NJ1 : 1];
+#pragma unroll
+            for (int i = 0; i < MI; ++i) aprev[i] = symtile::u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < NJ1; ++j) b1[j] = symtile::u32x4{0u, 0u, 0u, 0u};
+            auto mfmas1 = [&]() {
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ1; ++j) mma(i, NJ0 + j, aprev[i], b1[j]);
+            };
+            for (int kt = 0; kt < KT; ++kt) {
+                const int buf = kt % NS;
+                stage_ready(kt);
+#pragma unroll
+                for (int i = 0; i < MI; ++i) acur[i] = read_a(buf, i, lane >> 4);
+#pragma unroll
+                for (int j = 0; j < NJ0; ++j) b0[j] = read_b(buf, j, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                mfmas1();          // stage kt-1, group 1 (zeros when kt = 0)
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int j = 0; j < NJ1; ++j) b1[j] = read_b(buf, NJ0 + j, 0);
+                wait_lds<RD1>();
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NJ0; ++j) mma(i, j, acur[i], b0[j]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 0; i < MI; ++i) aprev[i] = acur[i];
+            }
+            wait_lds<0>();
+            mfmas1();              // last stage, group 1
         }
-        wait_lds<0>();
-        mfmas(a1, b1);             // last stage, substep 1
         __syncthreads();           // every wave is done with the ring
 
         // ---- epilogue: round, restage row-major, store, release --------
         uint8_t* Cs = smem;
-        constexpr int CROW = BN * 2;               // bytes per staged C row
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int row = wm * WM + i * 32 + (lane & 31);
-                    const int col = wn * WN + j * 32 + 8 * g + 4 * (lane >> 5);
+                for (int g = 0; g < ACC_N / 4; ++g) {
+                    // MF = 32: lane l, registers 4g..4g+3 hold row l % 32,
+                    // columns 8g + 4 * (l / 32) .. +3 of the block; MF = 16:
+                    // row l % 16, columns 4 * (l / 16) .. +3.
+                    const int row = wm * WM + i * MF + (lane % MF);
+                    const int col = wn * WN + j * MF +
+                                    ((MF == 32) ? 8 * g + 4 * (lane >> 5) : 4 * (lane >> 4));
                     uint2 w;
                     w.x = cvt_pack<BF16>(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
                     w.y = cvt_pack<BF16>(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
@@ -522,10 +608,10 @@ struct Variant {
     const void* scatter;
 };
 
-template <int BM, int BN, bool BF16, int NW>
+template <int BM, int BN, bool BF16, int NW, int MF = 32>
 Variant make_variant() {
     return Variant{BM, BN, BF16, NW,
-                   reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW>),
+                   reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF>),
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>)};
 }
 
@@ -538,6 +624,7 @@ const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
         make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
         make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
         make_variant<256, 128, false, 8>(),  make_variant<256, 128, true, 8>(),
+        make_variant<256, 224, false, 8, 16>(), make_variant<256, 224, true, 8, 16>(),
     };
     for (const Variant& v : table)
         if (v.bm == bm && v.bn == bn && v.bf16 == bf16 && (waves == 0 || v.waves == waves))

@@ -57,6 +57,10 @@ RAGGED = [
     (4, 130, 264, 72, 256, 128, "bf16"),
     (5, 257, 264, 520, 256, 256, "f16"),
     (8, 64, 8, 8, 64, 64, "bf16"),
+    # 256 x 224 tiles (16x16x32 MFMAs, B staged 256 wide): ragged rows,
+    # columns and K, and a column tail narrower than one 16-column block
+    (3, 300, 504, 200, 256, 224, "bf16"),
+    (2, 257, 232, 72, 256, 224, "f16"),
 ]
 
 
@@ -198,6 +202,24 @@ def test_full_size_variants_match_oracle_and_each_other(wl):
         p.barrier()
         check_gathered(p, want, flag_count=int(p.calls[0]))
         heaps[v] = u16(p.out.C(5))[:, :wl.N_local].copy()
+    assert np.array_equal(heaps[FUSED], heaps[WGSPEC])
+    assert np.array_equal(heaps[FUSED], heaps[BULK])
+
+
+def test_large_bf16_224_wide_tiles_match_oracle():
+    """256 x 224 tiles give the 4096 x 3584 output exactly 256 tiles; every
+    schedule matches the oracle and the three leave identical heaps."""
+    wl = workload.LARGE_BF16
+    p = Problem(wl.world, wl.M, wl.N_local, wl.K, wl.dtype, 256, 224, dist=wl.dist, seed=6)
+    assert p.out.tiles_n == 16 and p.out.tiles_m == 16
+    want = {3: oracle_block(p.A, p.shards[3], wl.dtype)}
+    heaps = {}
+    for v in (FUSED, WGSPEC, BULK):
+        p.sentinel()
+        p.run(3, v)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[3]))
+        heaps[v] = u16(p.out.C(0))[:, 3 * wl.N_local:4 * wl.N_local].copy()
     assert np.array_equal(heaps[FUSED], heaps[WGSPEC])
     assert np.array_equal(heaps[FUSED], heaps[BULK])
 
