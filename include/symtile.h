@@ -60,8 +60,8 @@ typedef enum { SYMTILE_SCOPE_BLOCK = 0, SYMTILE_SCOPE_GPU = 1,
  * documented defaults. */
 typedef struct {
     int variant;          /* symtile_variant */
-    int tile_m, tile_n;   /* output tile; (64,64) (128,128) (256,128) (256,256);
-                             0,0 = 256x256 */
+    int tile_m, tile_n;   /* output tile; (64,64) (128,128) (256,128) (256,256)
+                             (256,224); 0,0 = 256x256 */
     int gemm_wgs;         /* producer workgroups; 0 = min(tiles, CU count) for
                              BULK_SYNC/FUSED_SEQ, CU count - copy_wgs for WG_SPEC */
     int copy_wgs;         /* WG_SPEC consumers (0 = CU count / 8) and BULK_SYNC
@@ -71,11 +71,32 @@ typedef struct {
                              epoch after the call; 0 is taken as 1 */
     uint32_t spin_limit;  /* polls of one consumer wait before it gives up and
                              raises SYMTILE_ETIMEOUT; 0 = 1<<22 */
-    int nontemporal;      /* 1: streaming (non-temporal) stores of the output */
+    int nontemporal;      /* store policy of the output: 0 default, 1 streaming
+                             (non-temporal), 2 write-through (leaves no dirty L2
+                             line for the release to write back) */
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
-                             (8 for 256x256, 4 otherwise) */
+                             (8 for 256x256 and 256x224, 4 otherwise) */
+    uint64_t* trace;      /* optional per-tile timeline (Section 3.4, instrumentation):
+                             device uint64 [tiles_m*tiles_n][SYMTILE_TRACE_WORDS],
+                             tile (m, n) at row m*tiles_n + n; NULL = off.  See
+                             symtile_trace_word for the layout. */
 } symtile_gas_config;
+
+/* Per-tile trace record.  Times are ticks of the device's constant-rate
+ * realtime counter (symtile_clock_rate_khz), comparable across workgroups.
+ * Words a schedule has no event for are not written. */
+#define SYMTILE_TRACE_WORDS 8
+typedef enum {
+    SYMTILE_TRACE_START = 0,     /* producer picked the tile up */
+    SYMTILE_TRACE_MAINLOOP = 1,  /* accumulators final (K loop done, all waves) */
+    SYMTILE_TRACE_STORED = 2,    /* producer's stores acknowledged (all waves) */
+    SYMTILE_TRACE_RELEASED = 3,  /* producer's release fence and counter updates issued */
+    SYMTILE_TRACE_WHERE = 4,     /* producer location: HW_ID << 32 | XCC_ID << 16 | workgroup id */
+    SYMTILE_TRACE_COPY_WAIT = 5, /* WG_SPEC consumer starts waiting; BULK_SYNC copy start */
+    SYMTILE_TRACE_COPY_GO = 6,   /* WG_SPEC consumer acquired the ready counter; BULK_SYNC = word 5 */
+    SYMTILE_TRACE_COPY_DONE = 7  /* copy to the other slots stored and released */
+} symtile_trace_word;
 
 /* ---- heap (Section 3.2: constructor steps 3 and 6, host API table) -------- */
 
@@ -214,6 +235,9 @@ symtile_status symtile_gemm_all_scatter(symtile_heap* h, const void* A, const vo
                                         uint32_t* ready, int M, int N_local, int K, int lda,
                                         int ldb, int dtype, int rank, int world_size,
                                         const symtile_gas_config* cfg, symtile_stream s);
+
+/* Rate of the realtime counter behind trace timestamps, in kHz. */
+symtile_status symtile_clock_rate_khz(int device, int* khz);
 
 /* Number of compute units of `device` and the largest WG_SPEC grid
  * (gemm_wgs + copy_wgs) that is co-resident for the given tile shape. */

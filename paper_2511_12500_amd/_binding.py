@@ -39,7 +39,13 @@ class GasConfig(ctypes.Structure):
         ("nontemporal", ctypes.c_int),
         ("group_m", ctypes.c_int),
         ("waves_per_wg", ctypes.c_int),
+        ("trace", ctypes.c_void_p),
     ]
+
+
+TRACE_WORDS = 8   # SYMTILE_TRACE_WORDS
+(TRACE_START, TRACE_MAINLOOP, TRACE_STORED, TRACE_RELEASED, TRACE_WHERE, TRACE_COPY_WAIT,
+ TRACE_COPY_GO, TRACE_COPY_DONE) = range(8)
 
 
 def _load():
@@ -66,6 +72,7 @@ def _load():
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
     }
     for name, args in decl.items():
         f = getattr(L, name)
@@ -194,6 +201,13 @@ def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int
                                         dtype, rank, world_size,
                                         ctypes.byref(cfg) if cfg is not None else None,
                                         _vp(stream)), "symtile_gemm_all_scatter")
+
+
+def symtile_clock_rate_khz(device: int) -> int:
+    """Rate of the realtime counter behind trace timestamps, in kHz."""
+    khz = ctypes.c_int()
+    _check(lib.symtile_clock_rate_khz(device, ctypes.byref(khz)), "symtile_clock_rate_khz")
+    return khz.value
 
 
 def symtile_device_info(device: int, tile_m: int = 256, tile_n: int = 256):

@@ -77,7 +77,13 @@ struct GasParams {
     int group_m;
     uint32_t epoch, spin_limit;
     int nontemporal;
+    uint64_t* trace;        // [num_tiles][8] per-tile timeline, or nullptr
 };
+
+// Trace record of tile (tm, tn), or nullptr when tracing is off.
+__device__ __forceinline__ uint64_t* tile_trace(const GasParams& p, int tm, int tn) {
+    return p.trace ? p.trace + ((size_t)tm * p.tiles_n + tn) * SYMTILE_TRACE_WORDS : nullptr;
+}
 
 // s_waitcnt immediate that waits until at most n LDS (lgkm) operations of
 // this wave are outstanding; vmcnt and expcnt are left at their no-wait
@@ -199,9 +205,23 @@ __device__ __forceinline__ uint32_t tile_span(int rows_valid, int cols_valid, in
     return (uint32_t)(((size_t)(rows_valid - 1) * ldc + cols_valid) * 2);
 }
 
+// Store policy of the output (GasParams::nontemporal): 0 default, 1
+// non-temporal (streaming), 2 write-through (the L2 keeps no dirty line, so
+// the release fence that follows finds nothing of these stores to write
+// back).  Calls f with the cache-policy bits as a compile-time constant.
+template <typename F>
+__device__ __forceinline__ void with_store_policy(int mode, F&& f) {
+    if (mode == 1)
+        f(std::integral_constant<int, symtile::kStoreNonTemporal>{});
+    else if (mode == 2)
+        f(std::integral_constant<int, symtile::kStoreWriteThrough>{});
+    else
+        f(std::integral_constant<int, symtile::kStoreDefault>{});
+}
+
 // Copy one finished tile from the local heap to every other heap (the put of
 // Sections 4.1.1 and 4.2.2) and release its counters there.
-template <int BM, int BN, int THREADS, bool NT>
+template <int BM, int BN, int THREADS, int POLICY>
 __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
     using IO = TileIO<BM, BN, THREADS>;
     const int tid = threadIdx.x;
@@ -226,7 +246,7 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
                 symtile::make_rsrc(symtile::translate(src, p.rank, s, p.bases), span);
 #pragma unroll
             for (int u = 0; u < IO::U; ++u)
-                symtile::buf_st16<NT>(v[u], rd, voff, (b + u) * pass_bytes);
+                symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
         }
     }
     symtile::wg_stores_done();
@@ -290,21 +310,24 @@ void gas_kernel(const GasParams p) {
         for (int t = cid; t < p.num_tiles; t += p.copy_wgs) {
             int tm, tn;
             tile_coords(t, p.gemm_wgs, p, tm, tn);
+            uint64_t* tr = tile_trace(p, tm, tn);
             if (tid == 0) {
+                if (tr) tr[SYMTILE_TRACE_COPY_WAIT] = symtile::clock_now();
                 const bool ok =
                     symtile::flag_wait_geq(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
                 if (ok)
                     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
                 else
                     symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+                if (tr) tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
                 s_ok = ok;
             }
             __syncthreads();
             if (!s_ok) return;
-            if (p.nontemporal)
-                put_tile_to_peers<BM, BN, THREADS, true>(p, tm, tn);
-            else
-                put_tile_to_peers<BM, BN, THREADS, false>(p, tm, tn);
+            with_store_policy(p.nontemporal, [&](auto pol) {
+                put_tile_to_peers<BM, BN, THREADS, decltype(pol)::value>(p, tm, tn);
+            });
+            if (tr && tid == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
         }
         return;
     }
@@ -344,6 +367,13 @@ void gas_kernel(const GasParams p) {
     for (int t = pid; t < p.num_tiles; t += G) {
         int tm, tn;
         tile_coords(t, G, p, tm, tn);
+        // (the trace record's address is recomputed at each event so that
+        // nothing extra stays live across the K loop)
+        if (p.trace && tid == 0) {
+            uint64_t* tr = tile_trace(p, tm, tn);
+            tr[SYMTILE_TRACE_START] = symtile::clock_now();
+            tr[SYMTILE_TRACE_WHERE] = symtile::trace_location();
+        }
         const int m0 = tm * BM, n0 = tn * BN;
         const int rows_a = min(BM, p.M - m0);
         const symtile::i32x4_t rA = symtile::make_rsrc_words(
@@ -522,6 +552,7 @@ void gas_kernel(const GasParams p) {
             mfmas1();              // last stage, group 1
         }
         __syncthreads();           // every wave is done with the ring
+        if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
 
         // ---- epilogue: round, restage row-major, store, release --------
         uint8_t* Cs = smem;
@@ -565,24 +596,23 @@ void gas_kernel(const GasParams p) {
                 const int s = (p.rank + d) % p.world;
                 const symtile::rsrc_t rd =
                     symtile::make_rsrc(symtile::translate(tile_local, p.rank, s, p.bases), span);
-                if (p.nontemporal) {
+                with_store_policy(p.nontemporal, [&](auto pol) {
 #pragma unroll
                     for (int u = 0; u < IO::U; ++u)
-                        symtile::buf_st16<true>(v[u], rd, voff, (b + u) * pass_bytes);
-                } else {
-#pragma unroll
-                    for (int u = 0; u < IO::U; ++u)
-                        symtile::buf_st16<false>(v[u], rd, voff, (b + u) * pass_bytes);
-                }
+                        symtile::buf_st16p<decltype(pol)::value>(v[u], rd, voff,
+                                                                 (b + u) * pass_bytes);
+                });
             }
         }
         symtile::wg_stores_done();     // also orders the LDS reads above before reuse
         if (tid == 0) {
+            if (p.trace) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
             symtile::release_agent();
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
             for (int d = 0; d < n_dst; ++d)
                 symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
             if (p.role == ROLE_WG_SPEC) symtile::flag_add(p.ready + tm * p.tiles_n + tn);
+            if (p.trace) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
         }
     }
 }
@@ -592,10 +622,13 @@ template <int BM, int BN>
 __global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
     for (int t = blockIdx.x; t < p.num_tiles; t += gridDim.x) {
         const int tm = t / p.tiles_n, tn = t % p.tiles_n;
-        if (p.nontemporal)
-            put_tile_to_peers<BM, BN, kThreads, true>(p, tm, tn);
-        else
-            put_tile_to_peers<BM, BN, kThreads, false>(p, tm, tn);
+        uint64_t* tr = tile_trace(p, tm, tn);
+        if (tr && threadIdx.x == 0)
+            tr[SYMTILE_TRACE_COPY_WAIT] = tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
+        with_store_policy(p.nontemporal, [&](auto pol) {
+            put_tile_to_peers<BM, BN, kThreads, decltype(pol)::value>(p, tm, tn);
+        });
+        if (tr && threadIdx.x == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
     }
 }
 
@@ -716,6 +749,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     }
     if (cfg.variant == SYMTILE_WG_SPEC && !ready)
         return fail(SYMTILE_EINVAL, "WG_SPEC needs a ready counter array");
+    if (reinterpret_cast<uintptr_t>(cfg.trace) % 8)
+        return fail(SYMTILE_EINVAL, "trace must be 8-byte aligned");
 
     int cus = 0, limit = 0;
     if (symtile_status st = coresident_limit(v, h->device, &cus, &limit)) return st;
@@ -743,6 +778,9 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     p.epoch = cfg.epoch;
     p.spin_limit = cfg.spin_limit;
     p.nontemporal = cfg.nontemporal;
+    if (cfg.nontemporal < 0 || cfg.nontemporal > 2)
+        return fail(SYMTILE_EINVAL, "nontemporal must be 0, 1 or 2");
+    p.trace = cfg.trace;
     p.copy_wgs = 0;
 
     hipStream_t stream = static_cast<hipStream_t>(s);

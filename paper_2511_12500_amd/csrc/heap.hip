@@ -225,7 +225,16 @@ extern "C" {
 
 const char* symtile_last_error(void) { return g_last_error.c_str(); }
 
-const char* symtile_version(void) { return "symtile 0.1 (gfx950)"; }
+const char* symtile_version(void) { return "symtile 0.2 (gfx950)"; }
+
+symtile_status symtile_clock_rate_khz(int device, int* khz) {
+    if (!khz) return symtile_host::fail(SYMTILE_EINVAL, "khz is NULL");
+    int n = 0;
+    SYMTILE_HIP(hipGetDeviceCount(&n));
+    if (device < 0 || device >= n) return symtile_host::fail(SYMTILE_EINVAL, "bad device");
+    SYMTILE_HIP(hipDeviceGetAttribute(khz, hipDeviceAttributeWallClockRate, device));
+    return SYMTILE_OK;
+}
 
 symtile_status symtile_heap_create(int device, int world_size, size_t slot_bytes,
                                    symtile_heap** out) {

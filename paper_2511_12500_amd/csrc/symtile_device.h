@@ -238,6 +238,21 @@ __device__ __forceinline__ bool flag_wait_geq(const uint32_t* flag, uint32_t tar
     return false;
 }
 
+// ---- per-tile trace (Section 3.4, instrumentation) -----------------------
+// Timestamps come from the device's constant-rate realtime counter (100 MHz
+// on this GPU family; the rate is the HIP wall-clock rate attribute), which
+// every CU reads from the same source, so times taken by different
+// workgroups compare directly.
+__device__ __forceinline__ uint64_t clock_now() { return __builtin_amdgcn_s_memrealtime(); }
+
+// Where the calling wave runs: the raw HW_ID register in the high 32 bits,
+// XCC_ID in bits 16-31 and the workgroup id in bits 0-15.
+__device__ __forceinline__ uint64_t trace_location() {
+    const uint32_t hw = __builtin_amdgcn_s_getreg(4 | (31 << 11));    // HW_REG_HW_ID
+    const uint32_t xcc = __builtin_amdgcn_s_getreg(20 | (15 << 11));  // HW_REG_XCC_ID
+    return ((uint64_t)hw << 32) | ((uint64_t)(xcc & 0xFFFFu) << 16) | (blockIdx.x & 0xFFFFu);
+}
+
 // Device error word codes (OR-ed into the heap's error word).
 enum : uint32_t { ERR_TIMEOUT = 1u };
 

@@ -130,13 +130,21 @@ class GatheredOutput:
         return self.heap.slots_view(self.flag_off, (self.heap.world, self.tiles_m, self.tiles_n),
                                     torch.int32)
 
+    def new_trace(self) -> torch.Tensor:
+        """Zeroed per-tile trace buffer [tiles_m * tiles_n, 8] (int64, on the
+        heap's device); tile (m, n) is row m * tiles_n + n."""
+        return torch.zeros((self.tiles_m * self.tiles_n, B.TRACE_WORDS), dtype=torch.int64,
+                           device=f"cuda:{self.heap.device}")
+
     def run(self, A: torch.Tensor, B_shard: torch.Tensor, rank: int, variant: int,
             gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
             spin_limit: int = 0, epoch: int | None = None, stream: int | None = None,
-            waves_per_wg: int = 0) -> None:
+            waves_per_wg: int = 0, trace: torch.Tensor | None = None) -> None:
         """One call of rank ``rank`` (enqueued on the stream, asynchronous).
         For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
-        more than after the previous WG_SPEC call on these buffers."""
+        more than after the previous WG_SPEC call on these buffers.
+        ``trace``: optional int64 device tensor from new_trace(), filled with
+        the per-tile timeline of this call."""
         if A.dtype != self.dtype or B_shard.dtype != self.dtype:
             raise TypeError("A and B_shard must have the output dtype")
         if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):
@@ -147,10 +155,15 @@ class GatheredOutput:
             raise ValueError("shape mismatch")
         if variant == B.WG_SPEC:
             self.ready_epoch = self.ready_epoch + 1 if epoch is None else epoch
+        if trace is not None and (not trace.is_cuda or trace.dtype != torch.int64 or
+                                  not trace.is_contiguous() or
+                                  trace.numel() < self.tiles_m * self.tiles_n * B.TRACE_WORDS):
+            raise ValueError("trace must be a contiguous int64 device tensor from new_trace()")
         cfg = B.GasConfig(variant=variant, tile_m=self.tile_m, tile_n=self.tile_n,
                           gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, epoch=max(self.ready_epoch, 1),
                           spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
-                          waves_per_wg=waves_per_wg)
+                          waves_per_wg=waves_per_wg,
+                          trace=trace.data_ptr() if trace is not None else None)
         dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
         B.symtile_gemm_all_scatter(
             self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),

@@ -44,6 +44,26 @@ def trace_stats(path: str, kernel: str) -> dict:
     raise KeyError(f"no kernel matching {kernel!r} in {path}")
 
 
+def trace_last(path: str, kernel: str, last: int) -> dict:
+    """Durations (ns) of the last `last` dispatches of the first kernel whose
+    name matches, from a --kernel-trace run_kernel_trace.csv (dispatch
+    order = start time)."""
+    rx = re.compile(kernel)
+    rows = []
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if rx.search(row["Kernel_Name"]):
+                rows.append((int(row["Start_Timestamp"]), int(row["End_Timestamp"]),
+                             row["Kernel_Name"]))
+    if not rows:
+        raise KeyError(f"no kernel matching {kernel!r} in {path}")
+    rows.sort()
+    name = rows[0][2]
+    d = [e - s for s, e, n in rows if n == name][-last:]
+    return {"name": name, "calls": len(d), "avg_ns": statistics.fmean(d), "min_ns": min(d),
+            "max_ns": max(d)}
+
+
 def counter_per_dispatch(path: str, counter: str, kernel: str) -> tuple[float, int, str]:
     """Median over matching dispatches of the counter summed over instances."""
     rx = re.compile(kernel)
@@ -62,7 +82,10 @@ def counter_per_dispatch(path: str, counter: str, kernel: str) -> tuple[float, i
 
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--trace", required=True)
+    ap.add_argument("--trace", required=True,
+                    help="run_kernel_stats.csv, or run_kernel_trace.csv with --last")
+    ap.add_argument("--last", type=int, default=0,
+                    help="average only the last N dispatches (needs run_kernel_trace.csv)")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--kernel", required=True, help="regex of the kernel to summarise")
@@ -76,11 +99,11 @@ def main(argv=None) -> int:
     ap.add_argument("--out", required=True)
     a = ap.parse_args(argv)
 
-    t = trace_stats(a.trace, a.kernel)
+    t = trace_last(a.trace, a.kernel, a.last) if a.last else trace_stats(a.trace, a.kernel)
     lines = [f"# {a.title or t['name']}", "", "Produced by:", ""]
     lines += [f"    {c}" for c in a.command]
     lines += ["", f"- kernel: `{t['name']}`",
-              f"- calls: {t['calls']}",
+              f"- calls: {t['calls']}" + (f" (the last {a.last} dispatches)" if a.last else ""),
               f"- avg_ns: {t['avg_ns']:.0f}",
               f"- min_ns: {t['min_ns']:.0f}",
               f"- max_ns: {t['max_ns']:.0f}"]

@@ -337,3 +337,43 @@ def test_four_and_eight_wave_kernels_agree_bitwise(case):
         check_gathered(p, want, flag_count=int(p.calls[1 % world]))
         heaps.append(u16(p.out.C_all()).copy())
     assert np.array_equal(heaps[0], heaps[1])
+
+
+# ---------------------------------------------------------------- trace
+
+@pytest.mark.parametrize("variant", VARIANTS, ids=VNAMES.get)
+def test_trace_records_every_tile_in_causal_order(variant):
+    """Per-tile timeline: every tile has its producer events in order; a
+    WG_SPEC consumer acquires only after the producer's stores were
+    acknowledged; the bulk copy kernel starts after every producer released.
+    Tracing does not change the results."""
+    from paper_2511_12500_amd import trace as T
+    world, rank = 4, 1
+    p = Problem(world, 600, 520, 264, "bf16", 128, 128, seed=7)
+    want = {rank: oracle_block(p.A, p.shards[rank], "bf16")}
+    tr = p.out.new_trace()
+    p.sentinel()
+    p.run(rank, variant, trace=tr)
+    p.barrier()
+    check_gathered(p, want)
+    raw = tr.cpu().numpy().view(np.uint64)
+    assert raw.shape == (p.out.tiles_m * p.out.tiles_n, T.WORDS)
+    prod = raw[:, [T.START, T.MAINLOOP, T.STORED, T.RELEASED]]
+    assert np.all(prod > 0)
+    assert np.all(np.diff(prod.astype(np.int64), axis=1) >= 0)
+    where = raw[:, T.WHERE]
+    assert np.all((where & np.uint64(0xFFFF)) < 1024)                 # workgroup id
+    assert np.all(((where >> np.uint64(16)) & np.uint64(0xFFFF)) < 8)  # XCC id
+    copy = raw[:, [T.COPY_WAIT, T.COPY_GO, T.COPY_DONE]].astype(np.int64)
+    if variant == FUSED:
+        assert np.all(copy == 0)
+    else:
+        assert np.all(copy > 0) and np.all(np.diff(copy, axis=1) >= 0)
+        if variant == WGSPEC:
+            assert np.all(copy[:, 1] >= raw[:, T.STORED].astype(np.int64))
+        else:
+            assert copy[:, 0].min() >= raw[:, T.RELEASED].astype(np.int64).max()
+    khz = sym().symtile_clock_rate_khz(0)
+    t = T.decode(raw, khz)
+    s = T.summary(t)
+    assert s["tiles"] == raw.shape[0] and s["span_us"] > 0
