@@ -55,6 +55,49 @@ struct CopyParams {
     int band_lg_w;           // >= 0: each run is one rectangle, 1 << band_lg_w chunks wide
 };
 
+// Move `passes` passes of one 16-byte chunk per thread (pass b at byte
+// offset voff + b * pass_bytes in both resources), kBatch passes per batch.
+// Passes past the last one lie beyond the resources (zero loads, dropped
+// stores).  Software-pipelined: the loads of batch i+1 are issued before the
+// stores of batch i.  Loads and stores share one in-order completion
+// counter, so in the plain order (load i, store i, load i+1) the wait for
+// batch i+1's data would also wait for batch i's store acknowledgements; in
+// this order the wait before storing batch i leaves the newer loads and
+// stores in flight.  The loop body has no branch, so the compiler's waits
+// stay exact.
+template <int POLICY>
+__device__ __forceinline__ void copy_passes(symtile::rsrc_t rs, symtile::rsrc_t rd, uint32_t voff,
+                                            uint32_t pass_bytes, int passes) {
+    const int nb = (passes + kBatch - 1) / kBatch;
+    if (nb <= 0) return;
+    u32x4 x[kBatch], y[kBatch];      // batches alternate between x and y (no register moves)
+    auto load = [&](u32x4 (&v)[kBatch], int batch) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            v[u] = symtile::buf_ld16(rs, voff, (uint32_t)(batch * kBatch + u) * pass_bytes);
+    };
+    auto store = [&](const u32x4 (&v)[kBatch], int batch) {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            symtile::buf_st16p<POLICY>(v[u], rd, voff, (uint32_t)(batch * kBatch + u) * pass_bytes);
+    };
+    load(x, 0);
+    int i = 0;
+    for (; i + 2 < nb; i += 2) {     // batch i in x; batches i+1, i+2 exist
+        load(y, i + 1);
+        store(x, i);
+        load(x, i + 2);
+        store(y, i + 1);
+    }
+    if (i + 1 < nb) {
+        load(y, i + 1);
+        store(x, i);
+        store(y, i + 1);
+    } else {
+        store(x, i);
+    }
+}
+
 // Copy tile `tile` of source rank r to rank dst.  TC = 16-byte chunks per
 // tile row when it divides the thread count (thread t keeps chunk column
 // t % TC), or 0 for any other width.
@@ -84,14 +127,7 @@ __device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int ds
                                             : symtile::kOOB;
         const uint32_t pass_bytes = (uint32_t)(RP * p.ld_bytes);
         const int passes = (nrows + RP - 1) / RP;
-        for (int b = 0; b < passes; b += kBatch) {
-            u32x4 v[kBatch];
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u)
-                symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
-        }
+        copy_passes<POLICY>(rs, rd, voff, pass_bytes, passes);
     } else {
         const int total = nrows * p.tile_chunks;
         for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
@@ -132,14 +168,7 @@ __device__ __forceinline__ void copy_rect(const CopyParams& p, int r, int dst, i
                                         : symtile::kOOB;
     const uint32_t pass_bytes = (uint32_t)(rp * p.ld_bytes);
     const int passes = (nrows + rp - 1) / rp;
-    for (int b = 0; b < passes; b += kBatch) {
-        u32x4 v[kBatch];
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-            symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
-    }
+    copy_passes<POLICY>(rs, rd, voff, pass_bytes, passes);
 }
 
 template <int TC, int POLICY>
@@ -254,6 +283,19 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
         int lg = 0;
         while (((size_t)1 << lg) < width) ++lg;
         if (((size_t)1 << lg) <= (size_t)kThreads) p.band_lg_w = lg;
+    }
+    // Buffer offsets are 32-bit: a tile's rows plus the out-of-range passes
+    // that complete its last batch must stay below 2 GiB (the out-of-range
+    // offset marker), or an offset could wrap back into the tile.
+    {
+        size_t rows_per_pass = 0;
+        if (p.band_lg_w >= 0)
+            rows_per_pass = (size_t)kThreads >> p.band_lg_w;
+        else if (p.tile_chunks == 16 || p.tile_chunks == 32 || p.tile_chunks == 64)
+            rows_per_pass = (size_t)kThreads / p.tile_chunks;
+        if (rows_per_pass &&
+            ((size_t)tile_r + rows_per_pass * kBatch) * ld_bytes >= (size_t(1) << 31))
+            return fail(SYMTILE_EINVAL, "row stride too large for this tile shape");
     }
 
     int prev = -1;
