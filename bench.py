@@ -83,7 +83,7 @@ def parse_args(argv=None):
     ap.add_argument("--nontemporal", type=int, default=2,
                     help="output store policy: 0 default, 1 non-temporal, 2 write-through")
     ap.add_argument("--copy-tile", type=int, default=128)
-    ap.add_argument("--copy-iters", type=int, default=20)
+    ap.add_argument("--copy-iters", type=int, default=30)
     ap.add_argument("--copy-per-wg", type=int, default=0, help="tiles per workgroup (0 = auto)")
     ap.add_argument("--no-copy", action="store_true", help="skip the heap tile-copy leg")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -172,7 +172,7 @@ def bench_copy(args, torch, sym, workload):
         sym.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, sym.F32, t, t,
                               wl.shift, -1, flags, tiles_per_wg=args.copy_per_wg, stream=stream)
 
-    for _ in range(3):
+    for _ in range(200):      # past the clock ramp (see --warmup)
         launch()
     torch.cuda.synchronize()
     cold, warm = [], []

@@ -242,6 +242,9 @@ def test_heap_tile_copy_rejects_bad_arguments():
         (src, dst, 64, 64, 64, 9, 16, 16, 1, -1, flags),           # dtype
         (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, 2, flags),      # only_rank out of range
         (src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, src),       # flags overlap data
+        # one row with a 512 MiB stride: the out-of-range passes of a tile's
+        # last batch would wrap a 32-bit buffer offset
+        (src, dst, 1, 64, 1 << 27, pkg.F32, 1, 64, 1, -1, flags),
     ]
     with pytest.raises(pkg.SymtileError) as e:
         pkg.symtile_tile_copy(h, src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, flags, -1, s)
