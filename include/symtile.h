@@ -42,7 +42,9 @@ typedef enum { SYMTILE_F16 = 1, SYMTILE_BF16 = 2, SYMTILE_F32 = 3 } symtile_dtyp
 typedef enum {
     SYMTILE_BULK_SYNC = 0,   /* Section 4.1.1: GEMM kernel, then scatter kernel, one stream */
     SYMTILE_FUSED_SEQ = 1,   /* Section 4.2.1: each tile stored to every rank after its K loop */
-    SYMTILE_WG_SPEC = 2      /* Section 4.2.2: producer WGs compute, consumer WGs scatter */
+    SYMTILE_WG_SPEC = 2,     /* Section 4.2.2: producer WGs compute, consumer WGs scatter */
+    SYMTILE_UNFUSED_PC = 3   /* Section 4.1.2: a GEMM kernel and a copy kernel on two streams,
+                                CUs partitioned by their grid sizes, per-tile ready counters */
 } symtile_variant;
 
 /* Atomic verbs of the device API (Section 3.3.3, device API table). */
@@ -63,12 +65,14 @@ typedef struct {
     int tile_m, tile_n;   /* output tile; (64,64) (128,128) (256,128) (256,256)
                              (256,224); 0,0 = 256x256 */
     int gemm_wgs;         /* producer workgroups; 0 = min(tiles, CU count) for
-                             BULK_SYNC/FUSED_SEQ, CU count - copy_wgs for WG_SPEC */
-    int copy_wgs;         /* WG_SPEC consumers (0 = CU count / 8) and BULK_SYNC
-                             scatter-kernel workgroups (0 = CU count) */
-    uint32_t epoch;       /* WG_SPEC: consumers wait until ready[tile] >= epoch,
-                             so ready must hold epoch - 1 on entry and holds
-                             epoch after the call; 0 is taken as 1 */
+                             BULK_SYNC/FUSED_SEQ, CU count - copy_wgs for WG_SPEC
+                             and UNFUSED_PC */
+    int copy_wgs;         /* WG_SPEC and UNFUSED_PC consumers (0 = CU count / 8) and
+                             BULK_SYNC scatter-kernel workgroups (0 = CU count) */
+    uint32_t epoch;       /* WG_SPEC, UNFUSED_PC: consumers wait until
+                             ready[tile] >= epoch, so ready must hold epoch - 1
+                             on entry and holds epoch after the call; 0 is taken
+                             as 1 */
     uint32_t spin_limit;  /* polls of one consumer wait before it gives up and
                              raises SYMTILE_ETIMEOUT; 0 = 1<<22 */
     int nontemporal;      /* store policy of the output: 0 default, 1 streaming
@@ -77,6 +81,9 @@ typedef struct {
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
                              (8 for 256x256 and 256x224, 4 otherwise) */
+    symtile_stream copy_stream; /* UNFUSED_PC: stream of the copy kernel; NULL = a
+                             stream the heap creates on first use.  It must not
+                             be the call's stream. */
     uint64_t* trace;      /* optional per-tile timeline (Section 3.4, instrumentation):
                              device uint64 [tiles_m*tiles_n][SYMTILE_TRACE_WORDS],
                              tile (m, n) at row m*tiles_n + n; NULL = off.  See

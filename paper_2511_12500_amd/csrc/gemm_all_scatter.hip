@@ -59,6 +59,7 @@ constexpr int NS = 4;                  // pipeline stages (LDS ring)
 constexpr int PD = 3;                  // prefetch distance in stages (< NS)
 
 enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2 };
+// (UNFUSED_PC runs gas_kernel as WG_SPEC producers only, and consumer_kernel.)
 
 struct GasParams {
     const uint16_t* A;
@@ -258,6 +259,39 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
     }
 }
 
+// Consumer loop of the producer-consumer schedules (Sections 4.1.2 and
+// 4.2.2): consumer `cid` of `ncons` takes tiles cid, cid + ncons, ... in the
+// producers' tile order, waits (bounded) until the producer's ready counter
+// reaches the epoch, acquires, and puts the tile to the other heaps.  A
+// timed-out wait records ERR_TIMEOUT and ends this consumer.
+template <int BM, int BN, int THREADS>
+__device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
+    __shared__ int s_ok;
+    const int tid = threadIdx.x;
+    for (int t = cid; t < p.num_tiles; t += ncons) {
+        int tm, tn;
+        tile_coords(t, p.gemm_wgs, p, tm, tn);
+        uint64_t* tr = tile_trace(p, tm, tn);
+        if (tid == 0) {
+            if (tr) tr[SYMTILE_TRACE_COPY_WAIT] = symtile::clock_now();
+            const bool ok =
+                symtile::flag_wait_geq(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
+            if (ok)
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            else
+                symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+            if (tr) tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
+            s_ok = ok;
+        }
+        __syncthreads();
+        if (!s_ok) return;
+        with_store_policy(p.nontemporal, [&](auto pol) {
+            put_tile_to_peers<BM, BN, THREADS, decltype(pol)::value>(p, tm, tn);
+        });
+        if (tr && tid == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Producer tile shapes.  MF = 32: v_mfma_f32_32x32x16, waves in a 2 x (NW/2)
 // grid, each stage read as two k16 substeps.  MF = 16: v_mfma_f32_16x16x32
@@ -297,7 +331,6 @@ void gas_kernel(const GasParams p) {
     constexpr int ACC_N = (MF == 32) ? 16 : 4;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
-    __shared__ int s_ok;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -306,29 +339,7 @@ void gas_kernel(const GasParams p) {
 
     // ---------------- consumer workgroups (Section 4.2.2) -----------------
     if (p.role == ROLE_WG_SPEC && pid >= p.gemm_wgs) {
-        const int cid = pid - p.gemm_wgs;
-        for (int t = cid; t < p.num_tiles; t += p.copy_wgs) {
-            int tm, tn;
-            tile_coords(t, p.gemm_wgs, p, tm, tn);
-            uint64_t* tr = tile_trace(p, tm, tn);
-            if (tid == 0) {
-                if (tr) tr[SYMTILE_TRACE_COPY_WAIT] = symtile::clock_now();
-                const bool ok =
-                    symtile::flag_wait_geq(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
-                if (ok)
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                else
-                    symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
-                if (tr) tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
-                s_ok = ok;
-            }
-            __syncthreads();
-            if (!s_ok) return;
-            with_store_policy(p.nontemporal, [&](auto pol) {
-                put_tile_to_peers<BM, BN, THREADS, decltype(pol)::value>(p, tm, tn);
-            });
-            if (tr && tid == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
-        }
+        consume_tiles<BM, BN, THREADS>(p, pid - p.gemm_wgs, p.copy_wgs);
         return;
     }
 
@@ -632,6 +643,17 @@ __global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
     }
 }
 
+// Copy kernel of the unfused producer-consumer schedule (Section 4.1.2):
+// runs on its own stream next to the producer grid of gas_kernel, on CUs of
+// its own, so its workgroups are wide (16 waves keep many stores in flight).
+template <int BM>
+constexpr int consumer_threads() { return BM >= 128 ? 1024 : 256; }
+
+template <int BM, int BN>
+__global__ __launch_bounds__(consumer_threads<BM>()) void consumer_kernel(const GasParams p) {
+    consume_tiles<BM, BN, consumer_threads<BM>()>(p, blockIdx.x, gridDim.x);
+}
+
 // ---------------------------------------------------------------------------
 struct Variant {
     int bm, bn;
@@ -639,13 +661,17 @@ struct Variant {
     int waves;
     const void* gas;
     const void* scatter;
+    const void* consumer;
+    int consumer_threads;
 };
 
 template <int BM, int BN, bool BF16, int NW, int MF = 32>
 Variant make_variant() {
     return Variant{BM, BN, BF16, NW,
                    reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF>),
-                   reinterpret_cast<const void*>(&scatter_kernel<BM, BN>)};
+                   reinterpret_cast<const void*>(&scatter_kernel<BM, BN>),
+                   reinterpret_cast<const void*>(&consumer_kernel<BM, BN>),
+                   consumer_threads<BM>()};
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
@@ -701,7 +727,7 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     if (cfg.epoch == 0) cfg.epoch = 1;
     if (cfg.spin_limit == 0) cfg.spin_limit = 1u << 22;
     if (cfg.group_m <= 0) cfg.group_m = 4;
-    if (cfg.variant < SYMTILE_BULK_SYNC || cfg.variant > SYMTILE_WG_SPEC)
+    if (cfg.variant < SYMTILE_BULK_SYNC || cfg.variant > SYMTILE_UNFUSED_PC)
         return fail(SYMTILE_EINVAL, "unknown variant");
     if (dtype != SYMTILE_F16 && dtype != SYMTILE_BF16)
         return fail(SYMTILE_EUNSUPPORTED, "dtype must be SYMTILE_F16 or SYMTILE_BF16");
@@ -747,8 +773,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         if (f0 < c0 + c_bytes && c0 < f0 + flag_bytes)
             return fail(SYMTILE_EINVAL, "arrived_local overlaps C_gathered_local");
     }
-    if (cfg.variant == SYMTILE_WG_SPEC && !ready)
-        return fail(SYMTILE_EINVAL, "WG_SPEC needs a ready counter array");
+    if ((cfg.variant == SYMTILE_WG_SPEC || cfg.variant == SYMTILE_UNFUSED_PC) && !ready)
+        return fail(SYMTILE_EINVAL, "WG_SPEC and UNFUSED_PC need a ready counter array");
     if (reinterpret_cast<uintptr_t>(cfg.trace) % 8)
         return fail(SYMTILE_EINVAL, "trace must be 8-byte aligned");
 
@@ -807,6 +833,39 @@ extern "C" symtile_status symtile_gemm_all_scatter(
             p.copy_wgs = c;
             SYMTILE_HIP(hipLaunchKernel(v->scatter, dim3(c), dim3(kThreads), args, 0, stream));
         }
+        return SYMTILE_OK;
+    }
+
+    if (cfg.variant == SYMTILE_UNFUSED_PC) {
+        // Two grids side by side (Section 4.1.2): producers on `stream`,
+        // consumers on the copy stream.  With g + c <= CU count the consumers
+        // occupy at most c CUs, so g CUs stay free for the producers and the
+        // consumers' waits always end.  Fork/join events keep the call's
+        // stream semantics: the copy kernel starts after earlier work on
+        // `stream`, and later work on `stream` waits for it.
+        int c = cfg.copy_wgs > 0 ? cfg.copy_wgs : std::max(1, cus / 8);
+        int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : cus - c;
+        if (g <= 0 || c <= 0)
+            return fail(SYMTILE_EINVAL, "UNFUSED_PC needs gemm_wgs > 0 and copy_wgs > 0");
+        if (g + c > cus)
+            return fail(SYMTILE_EUNSUPPORTED,
+                        "gemm_wgs + copy_wgs = " + std::to_string(g + c) + " exceeds the " +
+                            std::to_string(cus) + " CUs the two grids partition");
+        hipStream_t cs = static_cast<hipStream_t>(cfg.copy_stream);
+        if (symtile_status st = symtile_host::aux_stream(h)) return st;
+        if (!cs) cs = h->aux_stream;
+        if (cs == stream) return fail(SYMTILE_EINVAL, "copy_stream is the call's stream");
+        p.gemm_wgs = g;
+        p.copy_wgs = std::min(c, ntiles);
+        p.role = ROLE_WG_SPEC;
+        void* args[] = {&p};
+        SYMTILE_HIP(hipEventRecord(h->ev_fork, stream));
+        SYMTILE_HIP(hipStreamWaitEvent(cs, h->ev_fork, 0));
+        SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(64 * v->waves), args, 0, stream));
+        SYMTILE_HIP(hipLaunchKernel(v->consumer, dim3(p.copy_wgs), dim3(v->consumer_threads),
+                                    args, 0, cs));
+        SYMTILE_HIP(hipEventRecord(h->ev_join, cs));
+        SYMTILE_HIP(hipStreamWaitEvent(stream, h->ev_join, 0));
         return SYMTILE_OK;
     }
 

@@ -212,6 +212,14 @@ symtile_status set_device(const symtile_heap* h, int* previous) {
     return SYMTILE_OK;
 }
 
+symtile_status aux_stream(symtile_heap* h) {
+    if (!h->aux_stream)
+        SYMTILE_HIP(hipStreamCreateWithFlags(&h->aux_stream, hipStreamNonBlocking));
+    if (!h->ev_fork) SYMTILE_HIP(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
+    if (!h->ev_join) SYMTILE_HIP(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
+    return SYMTILE_OK;
+}
+
 int cu_count(int device) {
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
@@ -253,6 +261,9 @@ symtile_status symtile_heap_destroy(symtile_heap* h) {
     if (hipDeviceSynchronize() != hipSuccess) st = symtile_host::fail(SYMTILE_EHIP, "sync failed");
     if (h->owns_memory && h->base) (void)hipFree(h->base);
     if (h->control) (void)hipFree(h->control);
+    if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+    if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    if (h->aux_stream) (void)hipStreamDestroy(h->aux_stream);
     delete h;
     return st;
 }

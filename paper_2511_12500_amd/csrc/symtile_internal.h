@@ -22,6 +22,11 @@ struct symtile_heap {
     uint64_t* dev_bases;         // device copy of host_bases (control block)
     uint32_t* dev_err;           // device error word (control block)
     void* control;               // the control allocation
+    // Second stream and fork/join events of the unfused producer-consumer
+    // schedule, created on first use (default priority) and destroyed with
+    // the heap.
+    hipStream_t aux_stream;
+    hipEvent_t ev_fork, ev_join;
 };
 
 namespace symtile_host {
@@ -46,5 +51,9 @@ bool in_slot(const symtile_heap* h, const void* p, size_t bytes, int rank);
 symtile_status set_device(const symtile_heap* h, int* previous);
 
 int cu_count(int device);
+
+// The heap's second stream and its fork/join events, created on first use on
+// the heap's device (which must be current).
+symtile_status aux_stream(symtile_heap* h);
 
 }  // namespace symtile_host

@@ -139,12 +139,14 @@ class GatheredOutput:
     def run(self, A: torch.Tensor, B_shard: torch.Tensor, rank: int, variant: int,
             gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
             spin_limit: int = 0, epoch: int | None = None, stream: int | None = None,
-            waves_per_wg: int = 0, trace: torch.Tensor | None = None) -> None:
+            waves_per_wg: int = 0, trace: torch.Tensor | None = None,
+            copy_stream: int | None = None) -> None:
         """One call of rank ``rank`` (enqueued on the stream, asynchronous).
         For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
         more than after the previous WG_SPEC call on these buffers.
         ``trace``: optional int64 device tensor from new_trace(), filled with
-        the per-tile timeline of this call."""
+        the per-tile timeline of this call.  ``copy_stream``: UNFUSED_PC's
+        copy-kernel stream (default: one the heap creates)."""
         if A.dtype != self.dtype or B_shard.dtype != self.dtype:
             raise TypeError("A and B_shard must have the output dtype")
         if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):
@@ -153,7 +155,7 @@ class GatheredOutput:
         K2, N = B_shard.shape
         if M != self.M or N != self.N_local or K2 != K:
             raise ValueError("shape mismatch")
-        if variant == B.WG_SPEC:
+        if variant in (B.WG_SPEC, B.UNFUSED_PC):
             self.ready_epoch = self.ready_epoch + 1 if epoch is None else epoch
         if trace is not None and (not trace.is_cuda or trace.dtype != torch.int64 or
                                   not trace.is_contiguous() or
@@ -162,7 +164,7 @@ class GatheredOutput:
         cfg = B.GasConfig(variant=variant, tile_m=self.tile_m, tile_n=self.tile_n,
                           gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, epoch=max(self.ready_epoch, 1),
                           spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
-                          waves_per_wg=waves_per_wg,
+                          waves_per_wg=waves_per_wg, copy_stream=copy_stream,
                           trace=trace.data_ptr() if trace is not None else None)
         dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
         B.symtile_gemm_all_scatter(

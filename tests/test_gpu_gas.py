@@ -13,9 +13,9 @@ from tests.gpu_util import (SENTINEL, Problem, check_block, check_gathered, orac
 
 pytestmark = pytest.mark.gpu
 
-BULK, FUSED, WGSPEC = 0, 1, 2
-VARIANTS = [BULK, FUSED, WGSPEC]
-VNAMES = {BULK: "bulk_sync", FUSED: "fused_seq", WGSPEC: "wg_spec"}
+BULK, FUSED, WGSPEC, UNFUSED = 0, 1, 2, 3
+VARIANTS = [BULK, FUSED, WGSPEC, UNFUSED]
+VNAMES = {BULK: "bulk_sync", FUSED: "fused_seq", WGSPEC: "wg_spec", UNFUSED: "unfused_pc"}
 
 
 @pytest.fixture(autouse=True)
@@ -196,14 +196,14 @@ def test_full_size_variants_match_oracle_and_each_other(wl):
     p = _large_case(wl)
     want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
     heaps = {}
-    for v in (FUSED, WGSPEC, BULK):
+    for v in (FUSED, WGSPEC, BULK, UNFUSED):
         p.sentinel()
         p.run(0, v)
         p.barrier()
         check_gathered(p, want, flag_count=int(p.calls[0]))
         heaps[v] = u16(p.out.C(5))[:, :wl.N_local].copy()
-    assert np.array_equal(heaps[FUSED], heaps[WGSPEC])
-    assert np.array_equal(heaps[FUSED], heaps[BULK])
+    for v in (WGSPEC, BULK, UNFUSED):
+        assert np.array_equal(heaps[FUSED], heaps[v]), VNAMES[v]
 
 
 def test_large_bf16_224_wide_tiles_match_oracle():
@@ -214,14 +214,14 @@ def test_large_bf16_224_wide_tiles_match_oracle():
     assert p.out.tiles_n == 16 and p.out.tiles_m == 16
     want = {3: oracle_block(p.A, p.shards[3], wl.dtype)}
     heaps = {}
-    for v in (FUSED, WGSPEC, BULK):
+    for v in (FUSED, WGSPEC, BULK, UNFUSED):
         p.sentinel()
         p.run(3, v)
         p.barrier()
         check_gathered(p, want, flag_count=int(p.calls[3]))
         heaps[v] = u16(p.out.C(0))[:, 3 * wl.N_local:4 * wl.N_local].copy()
-    assert np.array_equal(heaps[FUSED], heaps[WGSPEC])
-    assert np.array_equal(heaps[FUSED], heaps[BULK])
+    for v in (WGSPEC, BULK, UNFUSED):
+        assert np.array_equal(heaps[FUSED], heaps[v]), VNAMES[v]
 
 
 def test_large_bf16_wg_spec_split_sweep_bitwise():
@@ -272,6 +272,58 @@ def test_repeated_wg_spec_epochs_see_fresh_data():
         p.barrier()
         check_gathered(p, want)                     # counters == epoch, data complete
         assert p.out.ready.cpu().numpy().min() == epoch
+
+
+def test_unfused_two_streams_split_sweep_and_epochs():
+    """Unfused producer-consumer (Section 4.1.2): GEMM grid and copy grid on
+    two streams partition the CUs; every split, with the heap's own copy
+    stream or a caller's, leaves the heap bitwise equal to the fused kernel's,
+    and repeated calls advance the ready counters one epoch each."""
+    wl = workload.LARGE_BF16
+    pkg = sym()
+    cus, _ = pkg.symtile_device_info(0, wl.tile_m, wl.tile_n)
+    p = _large_case(wl, seed=9)
+    p.sentinel()
+    p.run(0, FUSED)
+    p.barrier()
+    ref = u16(p.out.C_all()).copy()
+    check_block(ref[0][:, :wl.N_local], oracle_block(p.A, p.shards[0], wl.dtype), wl.dtype,
+                "fused reference")
+    side = torch.cuda.Stream()
+    for i, copy_wgs in enumerate((8, 32, 64)):
+        p.sentinel()
+        p.run(0, UNFUSED, gemm_wgs=cus - copy_wgs, copy_wgs=copy_wgs,
+              copy_stream=side.cuda_stream if i == 1 else None)
+        p.barrier()
+        assert np.array_equal(u16(p.out.C_all()), ref), copy_wgs
+        assert p.out.ready.cpu().numpy().min() == i + 1
+    arr = p.out.arrived_all().cpu().numpy()
+    assert np.all(arr[:, 0] == int(p.calls[0])) and np.all(arr[:, 1:] == 0)
+
+
+def test_unfused_argument_errors():
+    pkg = sym()
+    p = Problem(2, 128, 128, 64, "f16", 64, 64, seed=7)
+    cus, _ = pkg.symtile_device_info(0, 64, 64)
+    with pytest.raises(pkg.SymtileError) as e:                 # grids exceed the CUs
+        p.out.run(p.dA, p.dB[0], 0, UNFUSED, gemm_wgs=cus, copy_wgs=1)
+    assert e.value.name == "EUNSUPPORTED"
+    s = torch.cuda.Stream().cuda_stream                         # a non-default stream
+    with pytest.raises(pkg.SymtileError) as e:                 # copy stream = call stream
+        p.out.run(p.dA, p.dB[0], 0, UNFUSED, copy_stream=s, stream=s)
+    assert e.value.name == "EINVAL"
+    p.heap.barrier()
+
+
+def test_unfused_consumer_timeout_is_reported_not_hung():
+    pkg = sym()
+    p = Problem(2, 128, 128, 64, "f16", 64, 64, seed=7)
+    p.out.ready_epoch = 5                   # the copy kernel waits for 6; producers bring 1
+    p.run(0, UNFUSED, spin_limit=2000)
+    with pytest.raises(pkg.SymtileError) as e:
+        p.heap.barrier()
+    assert e.value.name == "ETIMEOUT"
+    p.heap.barrier()
 
 
 def test_consumer_timeout_is_reported_not_hung():
@@ -369,7 +421,7 @@ def test_trace_records_every_tile_in_causal_order(variant):
         assert np.all(copy == 0)
     else:
         assert np.all(copy > 0) and np.all(np.diff(copy, axis=1) >= 0)
-        if variant == WGSPEC:
+        if variant in (WGSPEC, UNFUSED):
             assert np.all(copy[:, 1] >= raw[:, T.STORED].astype(np.int64))
         else:
             assert copy[:, 0].min() >= raw[:, T.RELEASED].astype(np.int64).max()
