@@ -115,6 +115,23 @@ __device__ __forceinline__ void ring_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// Ask the scheduler to interleave the LDS reads and MFMAs of the current
+// scheduling region one by one (R reads, M MFMAs; reads first when
+// READS_FIRST), so the reads issue in the shadow of the MFMAs instead of as
+// one burst.  The compiler's own waits before each MFMA stay exact (it tracks
+// which registers each read fills).
+template <int R, int M, bool READS_FIRST>
+__device__ __forceinline__ void interleave_reads_mfmas() {
+    constexpr int Q = R > M ? R : M;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        if (READS_FIRST && q < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        if (q < M) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);               // MFMA
+        if (!READS_FIRST && q < R) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 // XOR swizzle of the 16-byte chunk index inside a 64-byte staged A row.  A
 // fragment read has 16 consecutive rows per 256-byte bank window: the row's
 // bits 0-1 pick the 64-byte quarter, bits 2-3 permute the chunk within it.
@@ -456,10 +473,8 @@ void gas_kernel(const GasParams p) {
         // Pipeline over an LDS ring of NS stages of BK = 32, loads issued PD
         // stages ahead.  Each stage's fragment reads form two groups; the
         // loop is rotated so that the MFMAs of stage kt-1's second group
-        // issue right after the barrier, while the reads of stage kt's first
-        // group are in flight: no wave waits on LDS after a barrier.  Before
-        // each MFMA group a wave waits for exactly the older group of reads
-        // (LDS reads complete in order).  Loads into LDS are not tracked by
+        // issue right after the barrier, interleaved with the reads of stage
+        // kt's first group: no wave waits on LDS after a barrier.  Loads into LDS are not tracked by
         // the compiler: each wave waits for its own with vmcnt, leaving the
         // later stages' loads in flight, and the barrier then publishes the
         // stage.
@@ -509,14 +524,16 @@ void gas_kernel(const GasParams p) {
             for (int kt = 0; kt < KT; ++kt) {
                 const int buf = kt % NS;
                 stage_ready(kt);
+                // substep-0 reads of stage kt interleaved with the MFMAs of
+                // stage kt-1's substep 1 (zeros when kt = 0) ...
                 read_group(buf, 0, a0, b0);
-                __builtin_amdgcn_sched_barrier(0);
-                mfmas(a1, b1);     // stage kt-1, substep 1 (zeros when kt = 0)
-                __builtin_amdgcn_sched_barrier(0);
+                mfmas(a1, b1);
+                interleave_reads_mfmas<RD, MI * NI, true>();
+                // ... then substep-1 reads behind the substep-0 MFMAs (the
+                // reads overwrite a1/b1 only after the MFMAs that use them)
                 read_group(buf, 1, a1, b1);
-                wait_lds<RD>();
                 mfmas(a0, b0);
-                __builtin_amdgcn_sched_barrier(0);
+                interleave_reads_mfmas<RD, MI * NI, false>();
             }
             wait_lds<0>();
             mfmas(a1, b1);         // last stage, substep 1
@@ -545,17 +562,15 @@ void gas_kernel(const GasParams p) {
                 for (int i = 0; i < MI; ++i) acur[i] = read_a(buf, i, lane >> 4);
 #pragma unroll
                 for (int j = 0; j < NJ0; ++j) b0[j] = read_b(buf, j, 0);
-                __builtin_amdgcn_sched_barrier(0);
                 mfmas1();          // stage kt-1, group 1 (zeros when kt = 0)
-                __builtin_amdgcn_sched_barrier(0);
+                interleave_reads_mfmas<MI + 2 * NJ0, MI * NJ1, true>();
 #pragma unroll
                 for (int j = 0; j < NJ1; ++j) b1[j] = read_b(buf, NJ0 + j, 0);
-                wait_lds<RD1>();
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
 #pragma unroll
                     for (int j = 0; j < NJ0; ++j) mma(i, j, acur[i], b0[j]);
-                __builtin_amdgcn_sched_barrier(0);
+                interleave_reads_mfmas<RD1, MI * NJ0, false>();
 #pragma unroll
                 for (int i = 0; i < MI; ++i) aprev[i] = acur[i];
             }
