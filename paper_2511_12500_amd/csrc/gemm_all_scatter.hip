@@ -493,8 +493,14 @@ void gas_kernel(const GasParams p) {
             wait_lds<0>();         // the previous stage's last fragments are in registers
             ring_barrier();
             __builtin_amdgcn_sched_barrier(0);
-            // every wave is past stage kt-1: its slot takes stage kt+PD
+        };
+        // After the barrier every wave is past stage kt-1, so its ring slot
+        // can take stage kt+PD.  The loads are issued between the two MFMA
+        // groups of stage kt rather than right after the barrier, where they
+        // would delay the first MFMAs.
+        auto prefetch = [&](int kt) {
             if (kt + PD < KT) load_tile(kt + PD, (kt + PD) % NS);
+            __builtin_amdgcn_sched_barrier(0);
         };
 
 #pragma unroll
@@ -529,6 +535,7 @@ void gas_kernel(const GasParams p) {
                 read_group(buf, 0, a0, b0);
                 mfmas(a1, b1);
                 interleave_reads_mfmas<RD, MI * NI, true>();
+                prefetch(kt);
                 // ... then substep-1 reads behind the substep-0 MFMAs (the
                 // reads overwrite a1/b1 only after the MFMAs that use them)
                 read_group(buf, 1, a1, b1);
@@ -564,6 +571,7 @@ void gas_kernel(const GasParams p) {
                 for (int j = 0; j < NJ0; ++j) b0[j] = read_b(buf, j, 0);
                 mfmas1();          // stage kt-1, group 1 (zeros when kt = 0)
                 interleave_reads_mfmas<MI + 2 * NJ0, MI * NJ1, true>();
+                prefetch(kt);
 #pragma unroll
                 for (int j = 0; j < NJ1; ++j) b1[j] = read_b(buf, NJ0 + j, 0);
 #pragma unroll
