@@ -186,25 +186,50 @@ symtile_status symtile_atomic_exercise(symtile_heap* h, int op, int sem, int sco
                                        int n_threads, uint32_t operand, uint32_t compare,
                                        uint32_t* old_out, symtile_stream s);
 
-/* ---- heap tile copy (Section 3.3.2, pointer-based put) -------------------- */
+/* Message-passing litmus test of the flag protocol (Section 3.3.3, memory
+ * model).  pairs writer/reader workgroup pairs (pair p: writer rank p % w,
+ * reader rank (p + 1) % w, placed on different XCDs) run `rounds` rounds:
+ * the writer writes `words` uint32 of a round-specific pattern into the
+ * reader's slot at data_off + 4 * words * p, then publishes a counter in the
+ * reader's slot (flag_off + 8p) with an agent-scope release; the reader
+ * acquires it, checks every word, and acknowledges through a counter in the
+ * writer's slot (flag_off + 8p + 4).  ordered = 0 drops the release and
+ * acquire fences (relaxed counters only).  result (device, 2 uint32, zeroed
+ * by the caller) accumulates [0] words that did not hold the round's value
+ * when read and [1] rounds checked.  The counters must be zero on entry.
+ * Waits are bounded by spin_limit polls (0 = 1<<22); a timeout records
+ * ETIMEOUT for the next symtile_barrier.  EINVAL for bad sizes or regions;
+ * EUNSUPPORTED when 2*pairs exceeds the CU count (all must be resident). */
+symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_off, int pairs,
+                                 int rounds, int words, int ordered, uint32_t spin_limit,
+                                 uint32_t* result, symtile_stream s);
 
-/* For every source rank r (all ranks when only_rank < 0, else only_rank),
- * copy the rows x cols matrix at offset src_off of slot r, tile by tile
- * (tile_r x tile_c, ragged edge tiles included), to offset dst_off of slot
- * (r + shift) mod world through the translated destination address, then
- * release-publish (agent scope) one uint32 counter per tile at
- * flag_off + 4 * tile of the destination slot (tile = tr * tiles_c + tc).
+/* ---- heap tile copy (Section 3.3.2, pointer-based put and get) ------------ */
+
+/* Direction of symtile_tile_copy for executing rank r (Section 3.3.2 device
+ * API table): PUT copies r's own buffer into rank (r + shift) mod w's (the
+ * write is remote); GET copies rank (r - shift) mod w's buffer into r's own
+ * (the read is remote).  Both leave the same post-state. */
+typedef enum { SYMTILE_PUT = 0, SYMTILE_GET = 1 } symtile_copy_mode;
+
+/* For every executing rank r (all ranks when only_rank < 0, else only_rank),
+ * copy the rows x cols matrix at offset src_off of the source slot, tile by
+ * tile (tile_r x tile_c, ragged edge tiles included), to offset dst_off of
+ * the destination slot (PUT: source r, destination (r + shift) mod w; GET:
+ * source (r - shift) mod w, destination r; addresses reached by translating
+ * rank r's), then release-publish (agent scope) one uint32 counter per tile
+ * at flag_off + 4 * tile of the destination slot (tile = tr * tiles_c + tc).
  * Row stride `ld` elements; element size from dtype (2 or 4 bytes).  All
  * ranks run in one launch.  Each workgroup copies tiles_per_wg consecutive
  * (rank, tile) items and publishes their counters after one release
- * (0 = about two workgroups per CU).  Requirements: cols*esize, tile_c*esize
+ * (0 = about one workgroup per CU).  Requirements: cols*esize, tile_c*esize
  * and ld*esize multiples of 16; offsets 16-byte aligned; regions inside the
- * slot; the source and destination regions must not overlap.  EINVAL
- * otherwise. */
+ * slot; the source and destination regions must not overlap; (tile_r + the
+ * rows of kBatch passes) * ld*esize below 2 GiB.  EINVAL otherwise. */
 symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off, int rows,
                                  int cols, int ld, int dtype, int tile_r, int tile_c,
                                  int shift, int only_rank, size_t flag_off, int tiles_per_wg,
-                                 symtile_stream s);
+                                 int mode, symtile_stream s);
 
 /* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
 

@@ -71,7 +71,7 @@ def load_library(path: str):
     lib.oracle_place.restype = None
     lib.oracle_flags.argtypes = [p, i32, i32, i64, i64, ctypes.c_uint32]
     lib.oracle_flags.restype = None
-    lib.oracle_tile_copy.argtypes = [p, p, p, i32, i64, i64, i32, i64, i64, i32, i32]
+    lib.oracle_tile_copy.argtypes = [p, p, p, i32, i64, i64, i32, i64, i64, i32, i32, i32]
     lib.oracle_tile_copy.restype = None
     return lib
 
@@ -186,9 +186,11 @@ def gemm_all_scatter(state: GatheredState, A_bits: np.ndarray, B_bits: np.ndarra
 
 
 def tile_copy(send: np.ndarray, recv: np.ndarray, tile_r: int, tile_c: int,
-              shift: int = 1, only_rank: int = -1, lib=None):
+              shift: int = 1, only_rank: int = -1, lib=None, get: bool = False):
     """Expected (recv, copyflag) after every rank r (or only ``only_rank``)
-    copies send[r] to recv[(r + shift) mod w] tile by tile.  send/recv are
+    copies tile by tile, Section 3.3.2: put (default) sends send[r] to
+    recv[(r + shift) mod w]; get pulls send[(r - shift) mod w] into recv[r].
+    The counter of a tile is in the destination slot.  send/recv are
     [w, rows, cols]."""
     lib = lib or _load()
     send = np.ascontiguousarray(send)
@@ -198,5 +200,5 @@ def tile_copy(send: np.ndarray, recv: np.ndarray, tile_r: int, tile_c: int,
     world, rows, cols = send.shape
     flags = np.zeros((world, tiles(rows, tile_r) * tiles(cols, tile_c)), dtype=np.uint32)
     lib.oracle_tile_copy(_ptr(send), _ptr(out), _ptr(flags), world, rows, cols,
-                         send.dtype.itemsize, tile_r, tile_c, shift, only_rank)
+                         send.dtype.itemsize, tile_r, tile_c, shift, only_rank, int(get))
     return out, flags

@@ -158,19 +158,22 @@ void oracle_flags(uint32_t* arrived, int world, int rank,
  * incremented by one.  copyflag is [world][tiles]. */
 void oracle_tile_copy(const uint8_t* send, uint8_t* recv, uint32_t* copyflag,
                       int world, int64_t rows, int64_t cols, int esize,
-                      int64_t tile_r, int64_t tile_c, int shift, int only_rank) {
+                      int64_t tile_r, int64_t tile_c, int shift, int only_rank, int get) {
     const int64_t tiles_r = (rows + tile_r - 1) / tile_r;
     const int64_t tiles_c = (cols + tile_c - 1) / tile_c;
     const int64_t slot_bytes = rows * cols * esize;
     for (int r = 0; r < world; ++r) {
         if (only_rank >= 0 && r != only_rank) continue;
-        const int dst = ((r + shift) % world + world) % world;
+        /* put: rank r writes its send into rank r+shift's recv;
+           get: rank r reads rank r-shift's send into its own recv */
+        const int src = get ? ((r - shift) % world + world) % world : r;
+        const int dst = get ? r : ((r + shift) % world + world) % world;
         for (int64_t tr = 0; tr < tiles_r; ++tr)
             for (int64_t tc = 0; tc < tiles_c; ++tc) {
                 for (int64_t i = tr * tile_r; i < rows && i < (tr + 1) * tile_r; ++i)
                     for (int64_t j = tc * tile_c; j < cols && j < (tc + 1) * tile_c; ++j) {
                         const int64_t e = (i * cols + j) * esize;
-                        memcpy(recv + dst * slot_bytes + e, send + r * slot_bytes + e,
+                        memcpy(recv + dst * slot_bytes + e, send + src * slot_bytes + e,
                                (size_t)esize);
                     }
                 copyflag[(int64_t)dst * tiles_r * tiles_c + tr * tiles_c + tc] += 1u;

@@ -9,6 +9,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsymtile.
 
 F16, BF16, F32 = 1, 2, 3
 BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC = 0, 1, 2, 3
+PUT, GET = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}
 SEMS = {"relaxed": 0, "acquire": 1, "release": 2, "acq_rel": 3}
 SCOPES = {"block": 0, "gpu": 1, "sys": 2}
@@ -69,11 +70,13 @@ def _load():
         "symtile_barrier": [vp, vp],
         "symtile_heap_fill": [vp, i32, sz, sz, i32, vp],
         "symtile_atomic_exercise": [vp, i32, i32, i32, sz, i32, i32, i32, u32, u32, vp, vp],
-        "symtile_tile_copy": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, i32, vp],
+        "symtile_tile_copy": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, i32, i32,
+                              vp],
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
+        "symtile_litmus_mp": [vp, sz, sz, i32, i32, i32, i32, u32, vp, vp],
     }
     for name, args in decl.items():
         f = getattr(L, name)
@@ -187,9 +190,12 @@ def symtile_atomic_exercise(h: int, op: int, sem: int, scope: int, offset: int, 
 
 def symtile_tile_copy(h: int, src_off: int, dst_off: int, rows: int, cols: int, ld: int,
                       dtype: int, tile_r: int, tile_c: int, shift: int, only_rank: int,
-                      flag_off: int, tiles_per_wg: int = 0, stream: int = 0) -> None:
+                      flag_off: int, tiles_per_wg: int = 0, stream: int = 0,
+                      mode: int = 0) -> None:
+    """mode: PUT (0) or GET (1); the C argument order is ..., tiles_per_wg,
+    mode, stream."""
     _check(lib.symtile_tile_copy(_vp(h), src_off, dst_off, rows, cols, ld, dtype, tile_r, tile_c,
-                                 shift, only_rank, flag_off, tiles_per_wg, _vp(stream)),
+                                 shift, only_rank, flag_off, tiles_per_wg, mode, _vp(stream)),
            "symtile_tile_copy")
 
 
@@ -202,6 +208,13 @@ def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int
                                         dtype, rank, world_size,
                                         ctypes.byref(cfg) if cfg is not None else None,
                                         _vp(stream)), "symtile_gemm_all_scatter")
+
+
+def symtile_litmus_mp(h: int, data_off: int, flag_off: int, pairs: int, rounds: int,
+                      words: int, ordered: int, spin_limit: int, result: int,
+                      stream: int = 0) -> None:
+    _check(lib.symtile_litmus_mp(_vp(h), data_off, flag_off, pairs, rounds, words, ordered,
+                                 spin_limit, _vp(result), _vp(stream)), "symtile_litmus_mp")
 
 
 def symtile_clock_rate_khz(device: int) -> int:

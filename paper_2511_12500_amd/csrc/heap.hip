@@ -229,6 +229,83 @@ int cu_count(int device) {
 
 }  // namespace symtile_host
 
+
+// Message-passing litmus test of the flag protocol (Section 3.3.3, memory
+// model): pair p = workgroups 2p (writer, rank p % w) and 2p+1 (reader, rank
+// (p + 1) % w); consecutive workgroup ids land on different XCDs, whose L2s
+// are not coherent with each other.  Round i: the writer waits for ack >= i-1
+// (acquire), writes the round's pattern into the reader's slot, waits for its
+// stores and release-publishes ready = i; the reader waits for ready >= i
+// (acquire), checks every word, counts mismatches, and release-publishes
+// ack = i in the writer's slot.  The data words are plain stores and loads,
+// as the tile data of the GEMM and copy kernels are.  ordered = 0 drops the
+// fences (relaxed flags only), the unsynchronised form the protocol exists to
+// prevent; compiler barriers keep program order there, so what the test sees
+// is the hardware's.
+__device__ __forceinline__ uint32_t litmus_word(uint32_t round, uint32_t j) {
+    return (round * 0x9E3779B1u) ^ (j * 0x85EBCA77u) ^ 0x5bd1e995u;
+}
+
+__global__ __launch_bounds__(256) void litmus_mp_kernel(const uint64_t* bases, uint32_t* err,
+                                                        int world, uint64_t data_off,
+                                                        uint64_t flag_off, int rounds, int words,
+                                                        int ordered, uint32_t spin_limit,
+                                                        uint32_t* result) {
+    __shared__ int s_ok;
+    __shared__ uint32_t s_bad;
+    const int pair = blockIdx.x >> 1;
+    const bool writer = (blockIdx.x & 1) == 0;
+    const int wr = pair % world, rd = (pair + 1) % world;
+    const int me = writer ? wr : rd;
+    // every address is named in rank `me`'s heap and translated
+    uint32_t* data_me = reinterpret_cast<uint32_t*>(bases[me] + data_off) + (size_t)pair * words;
+    uint32_t* ready_me = reinterpret_cast<uint32_t*>(bases[me] + flag_off) + 2 * pair;
+    uint32_t* ack_me = ready_me + 1;
+    uint32_t* data = symtile::translate(data_me, me, rd, bases);   // the reader's buffer
+    uint32_t* ready = symtile::translate(ready_me, me, rd, bases);  // in the reader's slot
+    uint32_t* ack = symtile::translate(ack_me, me, wr, bases);      // in the writer's slot
+    const int tid = threadIdx.x;
+    if (tid == 0) s_bad = 0;
+    for (int i = 1; i <= rounds; ++i) {
+        if (tid == 0) {
+            const bool ok = writer ? symtile::flag_wait_geq(ack, (uint32_t)(i - 1), spin_limit)
+                                   : symtile::flag_wait_geq(ready, (uint32_t)i, spin_limit);
+            if (ok && ordered) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            if (!ok) symtile::raise_error(err, symtile::ERR_TIMEOUT);
+            s_ok = ok;
+        }
+        __syncthreads();
+        if (!s_ok) return;
+        asm volatile("" ::: "memory");
+        if (writer) {
+            for (int j = tid; j < words; j += blockDim.x)
+                *symtile::global_ptr(data + j) = litmus_word(i, j);
+            symtile::wg_stores_done();
+            if (tid == 0) {
+                if (ordered) symtile::release_agent();
+                symtile::flag_add(ready);
+            }
+        } else {
+            uint32_t bad = 0;
+            for (int j = tid; j < words; j += blockDim.x)
+                bad += *symtile::global_ptr(data + j) != litmus_word(i, j);
+            if (bad) atomicAdd(&s_bad, bad);
+            __syncthreads();                 // every word read before the ack
+            if (tid == 0) {
+                if (ordered) symtile::release_agent();
+                symtile::flag_add(ack);
+            }
+        }
+    }
+    __syncthreads();
+    if (tid == 0 && !writer) {
+        __hip_atomic_fetch_add(symtile::global_ptr(result), s_bad, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(symtile::global_ptr(result + 1), (uint32_t)rounds,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 extern "C" {
 
 const char* symtile_last_error(void) { return g_last_error.c_str(); }
@@ -387,6 +464,30 @@ symtile_status symtile_heap_fill(symtile_heap* h, int rank, size_t offset, size_
         }
         SYMTILE_HIP(hipGetLastError());
     }
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_off, int pairs,
+                                 int rounds, int words, int ordered, uint32_t spin_limit,
+                                 uint32_t* result, symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (pairs < 1 || pairs > 256 || rounds < 1 || words < 1 || words > (1 << 20))
+        return symtile_host::fail(SYMTILE_EINVAL, "pairs in [1, 256], rounds >= 1, words in [1, 2^20]");
+    if (!result) return symtile_host::fail(SYMTILE_EINVAL, "result is NULL");
+    const size_t data_bytes = (size_t)pairs * words * 4, flag_bytes = (size_t)pairs * 8;
+    if (data_off % 4 || flag_off % 4 || data_off > h->slot_stride ||
+        data_bytes > h->slot_stride - data_off || flag_off > h->slot_stride ||
+        flag_bytes > h->slot_stride - flag_off ||
+        (data_off < flag_off + flag_bytes && flag_off < data_off + data_bytes))
+        return symtile_host::fail(SYMTILE_EINVAL, "data or flags misaligned, outside the slot, or overlapping");
+    if (2 * pairs > symtile_host::cu_count(h->device))
+        return symtile_host::fail(SYMTILE_EUNSUPPORTED, "more workgroups than CUs (all must be resident)");
+    DeviceGuard guard(h->device);
+    hipLaunchKernelGGL(litmus_mp_kernel, dim3(2 * pairs), dim3(256), 0,
+                       static_cast<hipStream_t>(s), h->dev_bases, h->dev_err, h->world,
+                       (uint64_t)data_off, (uint64_t)flag_off, rounds, words, ordered ? 1 : 0,
+                       spin_limit ? spin_limit : (1u << 22), result);
+    SYMTILE_HIP(hipGetLastError());
     return SYMTILE_OK;
 }
 

@@ -1,7 +1,10 @@
-// Symmetric-heap tile copy: the pointer-based put of Section 3.3.2 applied
-// to every tile of a matrix, every emulated rank r sending to rank
-// (r + shift) mod w in one launch, with one release-published counter per
-// tile in the destination slot.
+// Symmetric-heap tile copy: the pointer-based put and get of Section 3.3.2
+// applied to every tile of a matrix, every emulated rank r taking part in one
+// launch.  Put: rank r copies its own buffer into rank (r + shift) mod w's.
+// Get: rank r copies rank (r - shift) mod w's buffer into its own.  Either
+// way one release-published counter per tile lands in the destination slot,
+// and the post-state is the same; what differs is which side's addresses are
+// translated (the remote read of a get, the remote write of a put).
 //
 // Data path: HBM-bound.  Each workgroup owns a run of tiles_per_wg
 // consecutive (rank, tile) items; every thread moves 16-byte chunks,
@@ -42,6 +45,7 @@ constexpr int kBatch = SYMTILE_COPY_BATCH;   // chunks in flight per thread
 struct CopyParams {
     const uint64_t* bases;
     int world, shift, only_rank;
+    int mode;                // SYMTILE_PUT or SYMTILE_GET
     uint64_t src_off, dst_off, flag_off;
     int rows;                // matrix rows
     int row_chunks;          // 16-byte chunks per matrix row
@@ -101,22 +105,32 @@ __device__ __forceinline__ void copy_passes(symtile::rsrc_t rs, symtile::rsrc_t 
 // Copy tile `tile` of source rank r to rank dst.  TC = 16-byte chunks per
 // tile row when it divides the thread count (thread t keeps chunk column
 // t % TC), or 0 for any other width.
+// Source and destination ranks of executing rank r.
+__device__ __forceinline__ void copy_ranks(const CopyParams& p, int r, int& src, int& dst) {
+    const int peer_up = ((r + p.shift) % p.world + p.world) % p.world;
+    const int peer_down = ((r - p.shift) % p.world + p.world) % p.world;
+    src = (p.mode == SYMTILE_GET) ? peer_down : r;
+    dst = (p.mode == SYMTILE_GET) ? r : peer_up;
+}
+
 template <int TC, int POLICY>
-__device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int dst, int tile) {
+__device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int src_rank, int dst,
+                                              int tile) {
     const int tr = tile / p.tiles_c, tc = tile - tr * p.tiles_c;
     const int row0 = tr * p.tile_r;
     const int chunk0 = tc * p.tile_chunks;
     const int nrows = min(p.tile_r, p.rows - row0);
     const int nchunks = min(p.tile_chunks, p.row_chunks - chunk0);
 
-    // The source is rank r's own buffer; the destination is the same
-    // symmetric object translated into the heap of rank dst.
+    // Both buffers are symmetric objects named by their address in rank r's
+    // heap, translated into the heaps of src_rank and dst.
     const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
                          (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
     const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
                                (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
     const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
-    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+    const symtile::rsrc_t rs =
+        symtile::make_rsrc(symtile::translate(src, r, src_rank, p.bases), span);
     const symtile::rsrc_t rd =
         symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
 
@@ -152,14 +166,15 @@ __device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int ds
 // a row (a row of up to W = 1 << lg_w chunks per pass group), so a run of
 // horizontally adjacent tiles streams whole row segments of up to 8 KiB.
 template <int POLICY>
-__device__ __forceinline__ void copy_rect(const CopyParams& p, int r, int dst, int row0,
+__device__ __forceinline__ void copy_rect(const CopyParams& p, int r, int src_rank, int dst, int row0,
                                           int chunk0, int nrows, int nchunks, int lg_w) {
     const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
                          (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
     const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
                                (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
     const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
-    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+    const symtile::rsrc_t rs =
+        symtile::make_rsrc(symtile::translate(src, r, src_rank, p.bases), span);
     const symtile::rsrc_t rd =
         symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
     const int c = threadIdx.x & ((1 << lg_w) - 1);
@@ -178,17 +193,19 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
     if (p.band_lg_w >= 0) {
         // The run is per_wg adjacent tiles of one tile row: one rectangle.
         const int r = p.only_rank >= 0 ? p.only_rank : first / p.ntiles;
-        const int dst = ((r + p.shift) % p.world + p.world) % p.world;
+        int src, dst;
+        copy_ranks(p, r, src, dst);
         const int t0 = first % p.ntiles;
         const int tr = t0 / p.tiles_c, tc = t0 - tr * p.tiles_c;
         const int row0 = tr * p.tile_r, chunk0 = tc * p.tile_chunks;
-        copy_rect<POLICY>(p, r, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
+        copy_rect<POLICY>(p, r, src, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
                       min(p.per_wg * p.tile_chunks, p.row_chunks - chunk0), p.band_lg_w);
     } else {
         for (int it = first; it < last; ++it) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
-            const int dst = ((r + p.shift) % p.world + p.world) % p.world;
-            copy_one_tile<TC, POLICY>(p, r, dst, it % p.ntiles);
+            int src, dst;
+            copy_ranks(p, r, src, dst);
+            copy_one_tile<TC, POLICY>(p, r, src, dst, it % p.ntiles);
         }
     }
     // Publish: every tile of the run is in its destination heap before any
@@ -198,7 +215,8 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
         symtile::release_agent();
         for (int it = first; it < last; ++it) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
-            const int dst = ((r + p.shift) % p.world + p.world) % p.world;
+            int src, dst;
+            copy_ranks(p, r, src, dst);
             uint32_t* flag_local =
                 reinterpret_cast<uint32_t*>(p.bases[r] + p.flag_off) + it % p.ntiles;
             symtile::flag_add(symtile::translate(flag_local, r, dst, p.bases));
@@ -211,7 +229,7 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
 extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off,
                                             int rows, int cols, int ld, int dtype, int tile_r,
                                             int tile_c, int shift, int only_rank,
-                                            size_t flag_off, int tiles_per_wg,
+                                            size_t flag_off, int tiles_per_wg, int mode,
                                             symtile_stream s) {
     using symtile_host::fail;
     if (!h) return fail(SYMTILE_EINVAL, "heap is NULL");
@@ -227,6 +245,8 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
         return fail(SYMTILE_EINVAL, "offsets misaligned (16 bytes for data, 4 for flags)");
     if (only_rank >= h->world) return fail(SYMTILE_EINVAL, "only_rank out of range");
     if (tiles_per_wg < 0) return fail(SYMTILE_EINVAL, "tiles_per_wg < 0");
+    if (mode != SYMTILE_PUT && mode != SYMTILE_GET)
+        return fail(SYMTILE_EINVAL, "mode must be SYMTILE_PUT or SYMTILE_GET");
     if (rows == 0 || cols == 0) return SYMTILE_OK;
     const size_t ld_bytes = (size_t)ld * esize;
     const size_t span = (size_t)(rows - 1) * ld_bytes + (size_t)cols * esize;
@@ -250,6 +270,7 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     p.world = h->world;
     p.shift = shift;
     p.only_rank = only_rank;
+    p.mode = mode;
     p.src_off = src_off;
     p.dst_off = dst_off;
     p.flag_off = flag_off;

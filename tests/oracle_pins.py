@@ -268,4 +268,22 @@ def pin_tile_copy(lib):
         assert np.all(flags1[dst] == 1) and np.all(flags1[others] == 0)
 
 
+def pin_tile_get(lib):
+    """Get (Section 3.3.2): rank r pulls slot r - shift into its own slot."""
+    rng = np.random.default_rng(23)
+    for (w, rows, cols, tr, tc, shift, dt) in ((8, 24, 40, 16, 8, 3, np.float32),
+                                               (3, 9, 17, 4, 8, 1, np.uint16)):
+        send = rng.integers(0, 2 ** 16, size=(w, rows, cols)).astype(dt)
+        recv = np.zeros_like(send)
+        out, flags = oracle.tile_copy(send, recv, tr, tc, shift, lib=lib, get=True)
+        assert np.array_equal(out.view(np.uint8), np.roll(send, shift, axis=0).view(np.uint8))
+        assert np.all(flags == 1)
+        me = 1
+        out1, flags1 = oracle.tile_copy(send, recv, tr, tc, shift, only_rank=me, lib=lib, get=True)
+        assert np.array_equal(out1[me].view(np.uint8), send[(me - shift) % w].view(np.uint8))
+        others = [s for s in range(w) if s != me]
+        assert np.all(out1[others].view(np.uint8) == 0)
+        assert np.all(flags1[me] == 1) and np.all(flags1[others] == 0)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

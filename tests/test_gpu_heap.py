@@ -182,9 +182,12 @@ def _copy_heap(pkg, world, rows, cols, dtype_t):
     return heap, src, dst, flags
 
 
+@pytest.mark.parametrize("mode", [0, 1], ids=["put", "get"])
 @pytest.mark.parametrize("tile,per_wg", [(64, 0), (128, 0), (256, 0), (128, 1), (64, 7)])
-def test_heap_tile_copy_workload_bitexact(tile, per_wg):
-    """All 8 ranks copy send -> recv of rank (r+1) mod 8, 2048 x 2048 fp32."""
+def test_heap_tile_copy_workload_bitexact(tile, per_wg, mode):
+    """All 8 ranks copy send -> recv of rank (r+1) mod 8, 2048 x 2048 fp32
+    (put: each rank writes the next rank's heap; get: each rank reads the
+    previous rank's heap)."""
     pkg = sym()
     wl = workload.HEAP_COPY
     heap, src, dst, flags = _copy_heap(pkg, wl.world, wl.rows, wl.cols, torch.float32)
@@ -192,20 +195,22 @@ def test_heap_tile_copy_workload_bitexact(tile, per_wg):
     heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(send.cuda())
     heap.slots_view(dst, (wl.rows, wl.cols), torch.int32).fill_(-1)
     pkg.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, pkg.F32, tile, tile,
-                          wl.shift, -1, flags, tiles_per_wg=per_wg, stream=pkg.current_stream())
+                          wl.shift, -1, flags, tiles_per_wg=per_wg, stream=pkg.current_stream(),
+                          mode=mode)
     heap.barrier()
     recv = heap.slots_view(dst, (wl.rows, wl.cols), torch.float32).cpu().numpy()
     ntiles = (wl.rows // tile) * (wl.cols // tile)
     fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
     want, want_flags = oracle.tile_copy(send.numpy(), np.full_like(send.numpy(), np.nan),
-                                        tile, tile, wl.shift)
+                                        tile, tile, wl.shift, get=bool(mode))
     assert np.array_equal(recv.view(np.uint32), want.view(np.uint32))
     assert np.array_equal(fl, want_flags.astype(np.int32))
 
 
+@pytest.mark.parametrize("mode", [0, 1], ids=["put", "get"])
 @pytest.mark.parametrize("case", [(5, 100, 72, 32, 24, 3, "bf16"), (3, 33, 20, 16, 8, 1, "f32"),
                                   (8, 64, 64, 64, 64, 7, "f16")])
-def test_heap_tile_copy_ragged_and_single_rank(case):
+def test_heap_tile_copy_ragged_and_single_rank(case, mode):
     pkg = sym()
     world, rows, cols, tr, tc, shift, dt = case
     tdt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dt]
@@ -221,12 +226,13 @@ def test_heap_tile_copy_ragged_and_single_rank(case):
         heap.slots_view(flags, (ntiles,), torch.int32).zero_()
         heap.slots_view(dst, (rows, cols), ival).zero_()
         pkg.symtile_tile_copy(heap.handle, src, dst, rows, cols, cols, code, tr, tc, shift,
-                              only, flags, tiles_per_wg=3, stream=pkg.current_stream())
+                              only, flags, tiles_per_wg=3, stream=pkg.current_stream(),
+                              mode=mode)
         heap.barrier()
         recv = heap.slots_view(dst, (rows, cols), ival).cpu().numpy()
         fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
         want, wf = oracle.tile_copy(send.numpy(), np.zeros_like(send.numpy()), tr, tc, shift,
-                                    only_rank=only)
+                                    only_rank=only, get=bool(mode))
         assert np.array_equal(recv, want), only
         assert np.array_equal(fl, wf.astype(np.int32)), only
 
@@ -253,4 +259,55 @@ def test_heap_tile_copy_rejects_bad_arguments():
         with pytest.raises(pkg.SymtileError) as e:
             pkg.symtile_tile_copy(h, *args, 0, s)
         assert e.value.name == "EINVAL", args
+    with pytest.raises(pkg.SymtileError) as e:                  # unknown direction
+        pkg.symtile_tile_copy(h, src, dst, 64, 64, 64, pkg.F32, 16, 16, 1, -1, flags, 0, s,
+                              mode=2)
+    assert e.value.name == "EINVAL"
+    heap.barrier()
+
+
+# ---------------------------------------------------------------- memory-model litmus
+
+def _litmus(pkg, heap, pairs, rounds, words, ordered):
+    data = heap.alloc(pairs * words * 4)
+    flags = heap.alloc(pairs * 8)               # fresh, zeroed counters
+    result = torch.zeros(2, dtype=torch.int32, device="cuda")
+    pkg.symtile_litmus_mp(heap.handle, data, flags, pairs, rounds, words, ordered, 0,
+                          result.data_ptr(), pkg.current_stream())
+    heap.barrier()
+    return [int(x) for x in result.cpu()]
+
+
+def test_litmus_message_passing_release_acquire_sees_every_word():
+    """Writer -> reader message passing across XCDs (Section 3.3.3): with an
+    agent-scope release before each counter update and an acquire after each
+    successful wait, no reader ever sees a word of an older round."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, rounds = _litmus(pkg, heap, pairs=32, rounds=300, words=2048, ordered=1)
+    assert rounds == 32 * 300
+    assert bad == 0
+
+
+def test_litmus_relaxed_form_terminates():
+    """Without the fences the protocol gives no guarantee; the test only
+    requires that every round completes (the stale-word count is reported)."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, rounds = _litmus(pkg, heap, pairs=32, rounds=300, words=2048, ordered=0)
+    assert rounds == 32 * 300
+    print(f"relaxed message passing: {bad} stale words of {32 * 300 * 2048}")
+
+
+def test_litmus_rejects_bad_arguments():
+    pkg = sym()
+    heap = pkg.Heap(2, 1 << 20)
+    data, flags = heap.alloc(4096), heap.alloc(64)
+    res = torch.zeros(2, dtype=torch.int32, device="cuda")
+    for args, name in (((data, flags, 0, 1, 16, 1), "EINVAL"),       # no pairs
+                       ((data, data, 1, 1, 16, 1), "EINVAL"),        # flags overlap data
+                       ((data, flags, 256, 1, 4, 1), "EUNSUPPORTED")):  # 512 WGs > CUs
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_litmus_mp(heap.handle, *args, 0, res.data_ptr(), pkg.current_stream())
+        assert e.value.name == name, args
     heap.barrier()

@@ -45,6 +45,10 @@ MUTANTS = [
     ("f16 subnormal exponent", "(uint32_t)(113 - shift) << 23", "(uint32_t)(112 - shift) << 23"),
     ("f16 sign dropped", "uint32_t sign = (uint32_t)(h >> 15) & 1u;", "uint32_t sign = 0u * h;"),
     ("copy ring reversed", "((r + shift) % world + world) % world", "((r - shift) % world + world) % world"),
+    ("get reads its own slot", "const int src = get ? ((r - shift) % world + world) % world : r;",
+     "const int src = r;"),
+    ("get writes the peer", "const int dst = get ? r : ((r + shift) % world + world) % world;",
+     "const int dst = ((r + shift) % world + world) % world;"),
     ("copy ragged tile edge dropped", "i < rows && i < (tr + 1) * tile_r", "i + 1 < rows && i < (tr + 1) * tile_r"),
     ("copy flag on source slot", "copyflag[(int64_t)dst * tiles_r * tiles_c", "copyflag[(int64_t)r * tiles_r * tiles_c"),
 ]
