@@ -122,18 +122,22 @@ __device__ __forceinline__ i32x4_t make_rsrc_words(const void* base, uint32_t by
 // load writes, so for a tracked one it drains every such load before any
 // later LDS read, including reads of other pipeline stages; with this form
 // the caller orders the load itself: s_waitcnt vmcnt, then a barrier, before
-// any wave reads the bytes.  M0 carries the LDS address (one wait state
-// between writing M0 and the load).
+// any wave reads the bytes.  M0 carries the LDS address; it is an input
+// operand, so the compiler writes it and knows it is in use.  The compiler's
+// hazard recognizer does not look inside inline assembly, so the statement
+// provides the wait states itself: a VALU write of an SGPR (readfirstlane,
+// or readlane when the compiler reloads a spilled SGPR) needs 5 wait states
+// before a vector memory instruction reads that SGPR (offset or descriptor),
+// and writing M0 needs 1 before the load reads it; s_nop 4 gives 5.
 __device__ __forceinline__ void buf_ld16_lds_async(const i32x4_t& r, uint32_t lds_addr,
                                                    uint32_t voff, uint32_t soff) {
     asm volatile(
-        "s_mov_b32 m0, %0\n\t"
-        "s_nop 0\n\t"
-        "buffer_load_dwordx4 %1, %2, %3 offen lds"
+        "s_nop 4\n\t"
+        "buffer_load_dwordx4 %0, %1, %2 offen lds"
         :
-        : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(r),
-          "s"(__builtin_amdgcn_readfirstlane(soff))
-        : "memory", "m0");
+        : "v"(voff), "s"(r), "s"(__builtin_amdgcn_readfirstlane(soff)),
+          "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+        : "memory");
 }
 
 // LDS byte address of a pointer into __shared__ memory.
