@@ -43,8 +43,11 @@ typedef enum {
     SYMTILE_BULK_SYNC = 0,   /* Section 4.1.1: GEMM kernel, then scatter kernel, one stream */
     SYMTILE_FUSED_SEQ = 1,   /* Section 4.2.1: each tile stored to every rank after its K loop */
     SYMTILE_WG_SPEC = 2,     /* Section 4.2.2: producer WGs compute, consumer WGs scatter */
-    SYMTILE_UNFUSED_PC = 3   /* Section 4.1.2: a GEMM kernel and a copy kernel on two streams,
+    SYMTILE_UNFUSED_PC = 3,  /* Section 4.1.2: a GEMM kernel and a copy kernel on two streams,
                                 CUs partitioned by their grid sizes, per-tile ready counters */
+    SYMTILE_WAVE_SPEC = 4    /* Section 4.2.3: each workgroup's compute waves store tiles
+                                locally and one extra wave copies the previous tile to the
+                                other slots during the next K loop (256x128 tiles) */
 } symtile_variant;
 
 /* Atomic verbs of the device API (Section 3.3.3, device API table). */

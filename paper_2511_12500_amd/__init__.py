@@ -11,7 +11,7 @@ itself imports without the library, so a fresh checkout can build it.
 _BINDING = (
     "ATOMIC_OPS", "BF16", "BULK_SYNC", "F16", "F32", "FUSED_SEQ", "GET", "LIB_PATH", "PUT",
     "SCOPES", "SEMS",
-    "TRACE_WORDS", "UNFUSED_PC", "WG_SPEC", "GasConfig", "SymtileError", "lib", "symtile_atomic_exercise",
+    "TRACE_WORDS", "UNFUSED_PC", "WAVE_SPEC", "WG_SPEC", "GasConfig", "SymtileError", "lib", "symtile_atomic_exercise",
     "symtile_barrier", "symtile_clock_rate_khz", "symtile_device_info",
     "symtile_gemm_all_scatter", "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
     "symtile_heap_destroy", "symtile_heap_fill", "symtile_heap_info", "symtile_heap_ptr",

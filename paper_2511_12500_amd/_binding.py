@@ -8,7 +8,7 @@ import os
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsymtile.so")
 
 F16, BF16, F32 = 1, 2, 3
-BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC = 0, 1, 2, 3
+BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC, WAVE_SPEC = 0, 1, 2, 3, 4
 PUT, GET = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}
 SEMS = {"relaxed": 0, "acquire": 1, "release": 2, "acq_rel": 3}

@@ -58,7 +58,7 @@ constexpr int kRowBytes = BK * 2;      // LDS bytes per staged A row (4 chunks o
 constexpr int NS = 4;                  // pipeline stages (LDS ring)
 constexpr int PD = 3;                  // prefetch distance in stages (< NS)
 
-enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2 };
+enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2, ROLE_WAVE_SPEC = 3 };
 // (UNFUSED_PC runs gas_kernel as WG_SPEC producers only, and consumer_kernel.)
 
 struct GasParams {
@@ -309,6 +309,123 @@ __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
     }
 }
 
+// Copy wave of the wave-specialised schedule (Section 4.2.3).  The compute
+// waves of the workgroup store each tile into the local slot only (except
+// the workgroup's last tile, which they store everywhere); this extra wave
+// copies the previous tile from the local slot to the w-1 other slots while
+// the compute waves run the next tile's K loop, then releases its counters
+// there.  s_barrier counts every wave of the workgroup, so the copy wave
+// takes part in exactly the compute waves' barriers: KT ring barriers and 3
+// epilogue barriers per tile, and copies a slice of the tile between them.
+// A slice must not hold the wave at a barrier waiting for memory (that would
+// stretch the compute waves' stage): row groups are loaded two intervals
+// before they are stored, into two register sets used alternately, and the
+// counters are published two intervals after the last store, when the
+// stores have been acknowledged.  Loads and stores share one in-order
+// counter, so each interval issues its load before its stores.  With fewer
+// barriers than that needs (small K) the wave stores each group as soon as
+// it is loaded.
+template <int BM, int BN, int POLICY>
+__device__ void copy_wave_tiles(const GasParams& p, int KT) {
+    constexpr int CPR = staged_width(BN) / 8;   // 16-byte chunks per tile row
+    constexpr int RPI = 64 / CPR;               // tile rows per wave-wide access
+    constexpr int GROUPS = BM / RPI;
+    constexpr int MAXW = SYMTILE_MAX_WORLD;
+    static_assert(64 % CPR == 0 && BM % RPI == 0 && GROUPS % 2 == 0, "copy wave split");
+    const int lane = threadIdx.x & 63;
+    const int G = p.gemm_wgs;
+    const int intervals = KT + 3;
+    const bool piped = intervals >= GROUPS + 4;
+    const uint32_t group_bytes = (uint32_t)RPI * p.ldc * 2;
+    int ptm = -1, ptn = -1;                     // tile waiting to be copied
+    for (int t = blockIdx.x; t < p.num_tiles; t += G) {
+        if (ptm >= 0) {
+            // the compute waves' local stores of this tile were released at
+            // workgroup scope before the barrier that ended it
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            if (p.trace && lane == 0) {
+                uint64_t* tr = tile_trace(p, ptm, ptn);
+                tr[SYMTILE_TRACE_COPY_WAIT] = tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
+            }
+        }
+        const int m0 = max(ptm, 0) * BM, n0 = max(ptn, 0) * BN;
+        const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
+        const uint16_t* src = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
+        const uint32_t span = ptm >= 0 ? tile_span(rows, cols, p.ldc) : 0u;
+        const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
+        symtile::rsrc_t rd[MAXW - 1];
+#pragma unroll
+        for (int d = 1; d < MAXW; ++d)
+            rd[d - 1] = symtile::make_rsrc(
+                symtile::translate(src, p.rank, (p.rank + d) % p.world, p.bases),
+                d < p.world ? span : 0u);
+        const int c = lane % CPR;
+        const uint32_t voff =
+            (8 * c < cols) ? (uint32_t)((lane / CPR) * p.ldc * 2 + c * 16) : symtile::kOOB;
+        auto store_group = [&](const symtile::u32x4& v, int g) {
+#pragma unroll
+            for (int d = 0; d < MAXW - 1; ++d)       // dropped past the world (empty resource)
+                symtile::buf_st16p<POLICY>(v, rd[d], voff, (uint32_t)g * group_bytes);
+        };
+        auto publish = [&]() {
+            __builtin_amdgcn_s_waitcnt(vm_wait(0));
+            if (lane == 0) {
+                symtile::release_agent();
+                uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + ptm) * p.tiles_n + ptn;
+                for (int d = 1; d < p.world; ++d)
+                    symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world,
+                                                         p.bases));
+                if (p.trace) tile_trace(p, ptm, ptn)[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
+            }
+        };
+        if (ptm >= 0 && piped) {
+            // interval b loads group b (b < GROUPS) and stores group b-2
+            symtile::u32x4 x = symtile::buf_ld16(rs, voff, 0u);
+            ring_barrier();
+            symtile::u32x4 y = symtile::buf_ld16(rs, voff, group_bytes);
+            ring_barrier();
+            for (int b = 2; b < GROUPS + 2; b += 2) {
+                const symtile::u32x4 x2 = b < GROUPS ? symtile::buf_ld16(rs, voff, b * group_bytes) : x;
+                store_group(x, b - 2);
+                x = x2;
+                ring_barrier();
+                const symtile::u32x4 y2 =
+                    b + 1 < GROUPS ? symtile::buf_ld16(rs, voff, (b + 1) * group_bytes) : y;
+                store_group(y, b - 1);
+                y = y2;
+                ring_barrier();
+            }
+            ring_barrier();                          // interval GROUPS + 2
+            publish();
+            ring_barrier();                          // interval GROUPS + 3
+            for (int b = GROUPS + 4; b < intervals; ++b) ring_barrier();
+        } else {
+            bool published = ptm < 0;
+            int g = 0;
+            const int per = (GROUPS + intervals - 1) / intervals;
+            for (int b = 0; b < intervals; ++b) {
+                if (!published) {
+                    for (int q = 0; q < per && g < GROUPS; ++q, ++g)
+                        store_group(symtile::buf_ld16(rs, voff, (uint32_t)g * group_bytes), g);
+                    if (g == GROUPS) {
+                        publish();
+                        published = true;
+                    }
+                }
+                ring_barrier();                      // the compute waves' barrier b
+            }
+        }
+        int tm, tn;
+        tile_coords(t, G, p, tm, tn);
+        if (t + G < p.num_tiles) {
+            ptm = tm;
+            ptn = tn;
+        } else {
+            ptm = -1;                                // the compute waves store the last tile everywhere
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Producer tile shapes.  MF = 32: v_mfma_f32_32x32x16, waves in a 2 x (NW/2)
 // grid, each stage read as two k16 substeps.  MF = 16: v_mfma_f32_16x16x32
@@ -319,8 +436,9 @@ __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
 // staged columns past BN are loaded but never read.  With NW = 8 two waves
 // share each SIMD, so one wave's MFMAs run while the other waits on LDS,
 // global loads or the barrier.
-template <int BM, int BN, bool BF16, int NW, int MF>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW / 4, NW / 4)))
+template <int BM, int BN, bool BF16, int NW, int MF, bool CW = false>
+__global__ __launch_bounds__(64 * (NW + CW))
+__attribute__((amdgpu_waves_per_eu(NW / 4 + CW, NW / 4 + CW)))
 void gas_kernel(const GasParams p) {
     constexpr int THREADS = 64 * NW;
     constexpr int WGM = (MF == 32) ? 2 : 4, WGN = NW / WGM;   // wave grid
@@ -363,6 +481,16 @@ void gas_kernel(const GasParams p) {
     // ---------------- producer workgroups ---------------------------------
     const int G = p.gemm_wgs;
     const int KT = (p.K + BK - 1) / BK;
+    if constexpr (CW) {
+        // the copy wave (Section 4.2.3); the test is made visibly uniform so
+        // that the compiler keeps the copy wave's addressing scalar
+        if (__builtin_amdgcn_readfirstlane(wave) == NW) {
+            with_store_policy(p.nontemporal, [&](auto pol) {
+                copy_wave_tiles<BM, BN, decltype(pol)::value>(p, KT);
+            });
+            return;
+        }
+    }
 
     // A: wave w, load u fills staged rows A_RPI*(NW*u + w) .. +A_RPI-1; lane
     // l lands at chunk l % 4 of row A_RPI*(NW*u + w) + l / 4 and fetches the
@@ -611,7 +739,10 @@ void gas_kernel(const GasParams p) {
                 }
         __syncthreads();
 
-        const int n_dst = (p.role == ROLE_FUSED) ? p.world : 1;
+        // FUSED: every slot.  WAVE_SPEC: the local slot (the copy wave does the
+        // rest during the next tile), except for this workgroup's last tile.
+        const int n_dst =
+            (p.role == ROLE_FUSED || (CW && t + G >= p.num_tiles)) ? p.world : 1;
         const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
         const uint16_t* tile_local = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
         const uint32_t span = tile_span(rows, cols, p.ldc);
@@ -686,15 +817,25 @@ struct Variant {
     const void* scatter;
     const void* consumer;
     int consumer_threads;
+    const void* gas_ws;          // wave-specialised kernel (NW compute waves + 1), or null
 };
 
-template <int BM, int BN, bool BF16, int NW, int MF = 32>
+// The copy-wave kernel is instantiated only for the shapes that use it.
+template <int BM, int BN, bool BF16, int NW, int MF, bool WS>
+const void* wave_spec_kernel() {
+    if constexpr (WS)
+        return reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF, true>);
+    else
+        return nullptr;
+}
+
+template <int BM, int BN, bool BF16, int NW, int MF = 32, bool WS = false>
 Variant make_variant() {
     return Variant{BM, BN, BF16, NW,
                    reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF>),
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>),
                    reinterpret_cast<const void*>(&consumer_kernel<BM, BN>),
-                   consumer_threads<BM>()};
+                   consumer_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>()};
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
@@ -705,12 +846,21 @@ const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
         make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),
         make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
         make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
-        make_variant<256, 128, false, 8>(),  make_variant<256, 128, true, 8>(),
+        make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 224, false, 8, 16>(), make_variant<256, 224, true, 8, 16>(),
     };
     for (const Variant& v : table)
         if (v.bm == bm && v.bn == bn && v.bf16 == bf16 && (waves == 0 || v.waves == waves))
             return &v;
+    return nullptr;
+}
+
+// The shape's build with a copy wave, or null.
+const Variant* find_wave_spec_variant(int bm, int bn, bool bf16) {
+    for (int w : {8, 4}) {
+        const Variant* v = find_variant(bm, bn, bf16, w);
+        if (v && v->gas_ws) return v;
+    }
     return nullptr;
 }
 
@@ -750,7 +900,7 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     if (cfg.epoch == 0) cfg.epoch = 1;
     if (cfg.spin_limit == 0) cfg.spin_limit = 1u << 22;
     if (cfg.group_m <= 0) cfg.group_m = 4;
-    if (cfg.variant < SYMTILE_BULK_SYNC || cfg.variant > SYMTILE_UNFUSED_PC)
+    if (cfg.variant < SYMTILE_BULK_SYNC || cfg.variant > SYMTILE_WAVE_SPEC)
         return fail(SYMTILE_EINVAL, "unknown variant");
     if (dtype != SYMTILE_F16 && dtype != SYMTILE_BF16)
         return fail(SYMTILE_EUNSUPPORTED, "dtype must be SYMTILE_F16 or SYMTILE_BF16");
@@ -856,6 +1006,21 @@ extern "C" symtile_status symtile_gemm_all_scatter(
             p.copy_wgs = c;
             SYMTILE_HIP(hipLaunchKernel(v->scatter, dim3(c), dim3(kThreads), args, 0, stream));
         }
+        return SYMTILE_OK;
+    }
+
+    if (cfg.variant == SYMTILE_WAVE_SPEC) {
+        // One extra wave per workgroup copies finished tiles (Section 4.2.3).
+        const Variant* ws = find_wave_spec_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16);
+        if (!ws)
+            return fail(SYMTILE_EUNSUPPORTED, "wave specialisation is built for 256x128 tiles");
+        int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : std::min(ntiles, cus);
+        g = std::min(g, ntiles);
+        p.gemm_wgs = g;
+        p.role = ROLE_WAVE_SPEC;
+        void* args[] = {&p};
+        SYMTILE_HIP(hipLaunchKernel(ws->gas_ws, dim3(g), dim3(64 * (ws->waves + 1)), args, 0,
+                                    stream));
         return SYMTILE_OK;
     }
 

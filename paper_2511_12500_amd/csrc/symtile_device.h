@@ -85,8 +85,11 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
                                              0x00020000);
 }
 
+// The scalar offset `soff` must be the same in every lane of the wave (it is
+// an SGPR operand); it is made uniform explicitly so that the compiler never
+// wraps the access in a per-lane loop when it cannot prove it.
 __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return __builtin_amdgcn_raw_buffer_load_b128(r, voff, __builtin_amdgcn_readfirstlane(soff), 0);
 }
 
 // Store cache policies (the cache-policy bits of the gfx9.4/9.5 store):
@@ -99,7 +102,8 @@ enum : int { kStoreDefault = 0, kStoreNonTemporal = 2, kStoreWriteThrough = 17 }
 
 template <int POLICY>
 __device__ __forceinline__ void buf_st16p(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, POLICY);
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, __builtin_amdgcn_readfirstlane(soff),
+                                           POLICY);
 }
 
 template <bool NT>

@@ -429,3 +429,68 @@ def test_trace_records_every_tile_in_causal_order(variant):
     t = T.decode(raw, khz)
     s = T.summary(t)
     assert s["tiles"] == raw.shape[0] and s["span_us"] > 0
+
+
+# ---------------------------------------------------------------- wave specialisation
+
+WAVESPEC = 4
+
+
+@pytest.mark.parametrize("case", [
+    # world, M, N_local, K, gemm_wgs, dtype
+    (8, 1024, 1024, 4096, 8, "bf16"),      # 32 tiles, 4 per workgroup
+    (4, 600, 520, 264, 3, "bf16"),         # ragged rows, columns and K; 5 tiles each
+    (2, 257, 136, 72, 1, "f16"),           # one workgroup, every tile through the copy wave
+], ids=lambda c: "w%d_m%d_n%d_k%d_g%d_%s" % c)
+def test_wave_spec_matches_fused_bitwise(case):
+    """Section 4.2.3: compute waves store each tile locally and one extra wave
+    copies the previous tile to the other slots during the next K loop; the
+    heap equals the fused kernel's bit for bit and matches the oracle."""
+    world, M, N, K, g, dtype = case
+    p = Problem(world, M, N, K, dtype, 256, 128, seed=11)
+    r = world - 1
+    want = {r: oracle_block(p.A, p.shards[r], dtype)}
+    p.sentinel()
+    p.run(r, FUSED, gemm_wgs=g)
+    p.barrier()
+    ref = u16(p.out.C_all()).copy()
+    p.sentinel()
+    tr = p.out.new_trace()
+    p.run(r, WAVESPEC, gemm_wgs=g, trace=tr)
+    p.barrier()
+    check_gathered(p, want)
+    assert np.array_equal(u16(p.out.C_all()), ref)
+    from paper_2511_12500_amd import trace as T
+    raw = tr.cpu().numpy().view(np.uint64).astype(np.int64)
+    copied = raw[:, T.COPY_DONE] > 0
+    # every workgroup's last tile is stored everywhere by its compute waves
+    assert int(copied.sum()) == raw.shape[0] - min(g, raw.shape[0])
+    assert np.all(raw[copied, T.COPY_GO] >= raw[copied, T.STORED])
+    assert np.all(raw[copied, T.COPY_DONE] >= raw[copied, T.COPY_GO])
+
+
+def test_wave_spec_large_and_k_zero():
+    wl = workload.LARGE_BF16
+    p = Problem(wl.world, wl.M, wl.N_local, wl.K, wl.dtype, 256, 128, dist=wl.dist, seed=12)
+    want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
+    p.sentinel()
+    p.run(0, WAVESPEC, gemm_wgs=112)            # 448 tiles, 4 per workgroup
+    p.barrier()
+    check_gathered(p, want)
+    z = Problem(2, 300, 136, 0, "bf16", 256, 128, A=torch.zeros(300, 0, dtype=torch.bfloat16),
+                shards=[torch.zeros(0, 136, dtype=torch.bfloat16)] * 2)
+    z.sentinel()
+    z.run(1, WAVESPEC, gemm_wgs=1)
+    z.barrier()
+    G = u16(z.out.C_all())
+    assert np.all(G[:, :, 136:] == 0) and np.all(G[:, :, :136] == SENTINEL)
+    assert np.all(z.out.arrived_all().cpu().numpy()[:, 1] == 1)
+
+
+def test_wave_spec_other_tiles_unsupported():
+    pkg = sym()
+    p = Problem(2, 128, 128, 64, "bf16", 128, 128, seed=7)
+    with pytest.raises(pkg.SymtileError) as e:
+        p.run(0, WAVESPEC)
+    assert e.value.name == "EUNSUPPORTED"
+    p.heap.barrier()
