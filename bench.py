@@ -76,7 +76,7 @@ def parse_args(argv=None):
     ap.add_argument("--warmup", type=int, default=150)
     ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
     ap.add_argument("--variant", default="fused_seq",
-                    choices=["bulk_sync", "fused_seq", "wg_spec", "unfused_pc"])
+                    choices=["bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec"])
     ap.add_argument("--tile", default="256x256")
     ap.add_argument("--gemm-wgs", type=int, default=0)
     ap.add_argument("--copy-wgs", type=int, default=0)
@@ -99,7 +99,7 @@ def bench_gas(args, torch, sym, workload):
     wl = workload.GEMM_WORKLOADS[args.workload]
     tm, tn = (int(x) for x in args.tile.split("x"))
     variant = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
-               "unfused_pc": sym.UNFUSED_PC}[args.variant]
+               "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[args.variant]
     A, B = workload.workload_inputs(wl, seed=0)
     dA, dB = A.cuda(), B.cuda()
     tiles = -(-wl.M // tm) * -(-wl.N_local // tn)

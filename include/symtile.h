@@ -189,6 +189,30 @@ symtile_status symtile_atomic_exercise(symtile_heap* h, int op, int sem, int sco
                                        int n_threads, uint32_t operand, uint32_t compare,
                                        uint32_t* old_out, symtile_stream s);
 
+/* Value-based verbs of the device API (Section 3.3.2, load and store). */
+typedef enum { SYMTILE_LOAD = 0, SYMTILE_STORE = 1 } symtile_value_op;
+
+/* Moves `bytes` between slot cur_rank and slot remote_rank, one 16-byte
+ * vector per device thread. The remote address is always found by
+ * translating the address of the same offset in slot cur_rank.
+ * - LOAD: each vector is read with the device `load` verb from
+ *   remote_rank's slot at src_off and written to cur_rank's own slot at
+ *   dst_off.
+ * - STORE: each vector is read from cur_rank's own slot at src_off and
+ *   written with the device `store` verb to remote_rank's slot at dst_off.
+ * Either way, the destination ends up holding a bitwise copy of the source.
+ * With nontemporal = 1 the destination writes are nontemporal.
+ * Arguments:
+ * - offsets must be 16-byte aligned, and bytes a multiple of 16;
+ * - both regions must lie inside the slot, and they must not overlap when
+ *   cur_rank == remote_rank;
+ * - otherwise, or for a bad op or rank, the call returns EINVAL.
+ * bytes = 0 launches nothing.
+ * The call is asynchronous on stream s, and memory ordering is relaxed. */
+symtile_status symtile_value_exercise(symtile_heap* h, int op, size_t src_off, size_t dst_off,
+                                      size_t bytes, int cur_rank, int remote_rank,
+                                      int nontemporal, symtile_stream s);
+
 /* Message-passing litmus test of the flag protocol (Section 3.3.3, memory
  * model).  pairs writer/reader workgroup pairs (pair p: writer rank p % w,
  * reader rank (p + 1) % w, placed on different XCDs) run `rounds` rounds:

@@ -10,6 +10,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsymtile.
 F16, BF16, F32 = 1, 2, 3
 BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC, WAVE_SPEC = 0, 1, 2, 3, 4
 PUT, GET = 0, 1
+LOAD, STORE = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}
 SEMS = {"relaxed": 0, "acquire": 1, "release": 2, "acq_rel": 3}
 SCOPES = {"block": 0, "gpu": 1, "sys": 2}
@@ -77,6 +78,7 @@ def _load():
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
         "symtile_litmus_mp": [vp, sz, sz, i32, i32, i32, i32, u32, vp, vp],
+        "symtile_value_exercise": [vp, i32, sz, sz, sz, i32, i32, i32, vp],
     }
     for name, args in decl.items():
         f = getattr(L, name)
@@ -186,6 +188,15 @@ def symtile_atomic_exercise(h: int, op: int, sem: int, scope: int, offset: int, 
     _check(lib.symtile_atomic_exercise(_vp(h), op, sem, scope, offset, from_rank, to_rank,
                                        n_threads, operand & 0xFFFFFFFF, compare & 0xFFFFFFFF,
                                        _vp(old_out), _vp(stream)), "symtile_atomic_exercise")
+
+
+def symtile_value_exercise(h: int, op: int, src_off: int, dst_off: int, nbytes: int,
+                           cur_rank: int, remote_rank: int, nontemporal: int = 0,
+                           stream: int = 0) -> None:
+    """op: LOAD (0) or STORE (1)."""
+    _check(lib.symtile_value_exercise(_vp(h), op, src_off, dst_off, nbytes, cur_rank,
+                                      remote_rank, nontemporal, _vp(stream)),
+           "symtile_value_exercise")
 
 
 def symtile_tile_copy(h: int, src_off: int, dst_off: int, rows: int, cols: int, ld: int,

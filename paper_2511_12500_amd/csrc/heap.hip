@@ -55,6 +55,23 @@ __global__ void fill1_kernel(uint8_t* __restrict__ p, size_t n, uint8_t value) {
         p[i] = value;
 }
 
+// Value verbs (Section 3.3.2): one 16-byte vector per thread.  `own` is the
+// executing rank's slot base; the remote side is reached by translation.
+__global__ void value_exercise_kernel(char* own, const uint64_t* __restrict__ bases, int op,
+                                      int cur, int remote, uint64_t src_off, uint64_t dst_off,
+                                      size_t n16, int nontemporal) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n16;
+         i += (size_t)gridDim.x * blockDim.x) {
+        char* src = own + src_off + 16 * i;
+        char* dst = own + dst_off + 16 * i;
+        if (op == SYMTILE_LOAD) {
+            symtile::st16(dst, symtile::load(src, cur, remote, bases), nontemporal != 0);
+        } else {
+            symtile::store(dst, symtile::ld16(src), cur, remote, bases, nontemporal != 0);
+        }
+    }
+}
+
 // One atomic verb with compile-time order and scope.
 template <int SEM, int SCOPE>
 __device__ uint32_t apply_atomic(int op, uint32_t* p, uint32_t v, uint32_t cmp) {
@@ -487,6 +504,36 @@ symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_o
                        static_cast<hipStream_t>(s), h->dev_bases, h->dev_err, h->world,
                        (uint64_t)data_off, (uint64_t)flag_off, rounds, words, ordered ? 1 : 0,
                        spin_limit ? spin_limit : (1u << 22), result);
+    SYMTILE_HIP(hipGetLastError());
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_value_exercise(symtile_heap* h, int op, size_t src_off, size_t dst_off,
+                                      size_t bytes, int cur_rank, int remote_rank,
+                                      int nontemporal, symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (op != SYMTILE_LOAD && op != SYMTILE_STORE)
+        return symtile_host::fail(SYMTILE_EINVAL, "op must be SYMTILE_LOAD or SYMTILE_STORE");
+    if (cur_rank < 0 || cur_rank >= h->world || remote_rank < 0 || remote_rank >= h->world)
+        return symtile_host::fail(SYMTILE_EINVAL, "rank out of range");
+    if (nontemporal != 0 && nontemporal != 1)
+        return symtile_host::fail(SYMTILE_EINVAL, "nontemporal must be 0 or 1");
+    if (src_off % 16 || dst_off % 16 || bytes % 16)
+        return symtile_host::fail(SYMTILE_EINVAL, "offsets and bytes must be multiples of 16");
+    if (src_off > h->slot_stride || bytes > h->slot_stride - src_off ||
+        dst_off > h->slot_stride || bytes > h->slot_stride - dst_off)
+        return symtile_host::fail(SYMTILE_EINVAL, "region outside the slot");
+    if (cur_rank == remote_rank && src_off < dst_off + bytes && dst_off < src_off + bytes)
+        return symtile_host::fail(SYMTILE_EINVAL, "source and destination overlap in one slot");
+    if (bytes == 0) return SYMTILE_OK;
+    DeviceGuard guard(h->device);
+    const size_t n16 = bytes / 16;
+    unsigned grid = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
+    hipLaunchKernelGGL(value_exercise_kernel, dim3(grid), dim3(256), 0,
+                       static_cast<hipStream_t>(s),
+                       reinterpret_cast<char*>(h->host_bases[cur_rank]), h->dev_bases, op,
+                       cur_rank, remote_rank, (uint64_t)src_off, (uint64_t)dst_off, n16,
+                       nontemporal);
     SYMTILE_HIP(hipGetLastError());
     return SYMTILE_OK;
 }

@@ -106,11 +106,6 @@ __device__ __forceinline__ void buf_st16p(u32x4 v, rsrc_t r, uint32_t voff, uint
                                            POLICY);
 }
 
-template <bool NT>
-__device__ __forceinline__ void buf_st16(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-    buf_st16p<NT ? kStoreNonTemporal : kStoreDefault>(v, r, voff, soff);
-}
-
 // Descriptor words of the same buffer resource, for inline assembly.
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ i32x4_t make_rsrc_words(const void* base, uint32_t bytes) {
@@ -147,14 +142,6 @@ __device__ __forceinline__ void buf_ld16_lds_async(const i32x4_t& r, uint32_t ld
 // LDS byte address of a pointer into __shared__ memory.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// 16 bytes per lane from the buffer straight into LDS: lane l of the wave
-// writes lds_base + 16 * l (lds_base is wave-uniform).
-__device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* lds_base, uint32_t voff,
-                                             uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        r, (__attribute__((address_space(3))) void*)lds_base, 16, voff, soff, 0, 0);
 }
 
 // Every pointer in the heap is device (global) memory.  Atomics through a

@@ -1,5 +1,6 @@
 """GPU tests of the symmetric heap, translation (device vs host twin), the
-atomic verbs of the device API, and the heap tile copy (bit-exact vs oracle)."""
+atomic and value (load/store) verbs of the device API, and the heap tile
+copy (bit-exact vs oracle)."""
 import ctypes
 
 import numpy as np
@@ -168,6 +169,70 @@ def test_atomic_verbs_results():
     assert final == 50
     final, _ = _atomic(pkg, heap, "max", "acquire", "gpu", n, 50, 200)
     assert final == 50 + n - 1
+
+
+# ---------------------------------------------------------------- value verbs (device API)
+
+def _value_heap(pkg, world, nbytes, seed):
+    """Heap with every slot filled with seeded random bytes; returns the
+    heap, the region offsets and the host copy of every slot before the call."""
+    heap = pkg.Heap(world, 3 * nbytes + 4096)
+    src, dst = heap.alloc(nbytes + 64, 256), heap.alloc(nbytes + 64, 256)
+    g = torch.Generator().manual_seed(seed)
+    span = dst + nbytes + 64
+    before = torch.randint(0, 256, (world, span), generator=g, dtype=torch.uint8)
+    heap.slots_view(0, (span,), torch.uint8).copy_(before.cuda())
+    return heap, src, dst, before.numpy(), span
+
+
+@pytest.mark.parametrize("op", ["load", "store"])
+@pytest.mark.parametrize("nbytes,nt", [(16, 0), (4096, 1), (3 * 4096 * 256 + 48, 0),
+                                       (16 * 4096 * 256 + 16 * 77, 1)])
+def test_value_verbs_move_bitwise_copies(op, nbytes, nt):
+    pkg = sym()
+    world, cur, remote = 5, 1, 3
+    heap, src, dst, before, span = _value_heap(pkg, world, nbytes, seed=nbytes + nt)
+    pkg.symtile_value_exercise(heap.handle, pkg.LOAD if op == "load" else pkg.STORE, src, dst,
+                               nbytes, cur, remote, nt, pkg.current_stream())
+    heap.barrier()
+    after = heap.slots_view(0, (span,), torch.uint8).cpu().numpy()
+    want = before.copy()
+    # load: remote's source lands in cur's destination; store: the reverse
+    rd, wr = (remote, cur) if op == "load" else (cur, remote)
+    want[wr, dst:dst + nbytes] = before[rd, src:src + nbytes]
+    assert np.array_equal(after, want)
+
+
+def test_value_verbs_same_slot_and_empty():
+    pkg = sym()
+    heap, src, dst, before, span = _value_heap(pkg, 2, 1024, seed=3)
+    pkg.symtile_value_exercise(heap.handle, pkg.STORE, src, dst, 1024, 0, 0, 0,
+                               pkg.current_stream())
+    pkg.symtile_value_exercise(heap.handle, pkg.LOAD, src, dst, 0, 1, 0, 0,
+                               pkg.current_stream())
+    heap.barrier()
+    after = heap.slots_view(0, (span,), torch.uint8).cpu().numpy()
+    want = before.copy()
+    want[0, dst:dst + 1024] = before[0, src:src + 1024]
+    assert np.array_equal(after, want)
+
+
+def test_value_verbs_reject_bad_arguments():
+    pkg = sym()
+    heap = pkg.Heap(4, 1 << 20)
+    off = heap.alloc(1 << 16)
+    st = pkg.current_stream()
+    good = dict(op=pkg.LOAD, src=off, dst=off + 4096, n=1024, cur=0, remote=2, nt=0)
+    bad = [dict(op=2), dict(src=off + 8), dict(dst=off + 4100), dict(n=1000), dict(cur=4),
+           dict(remote=-1), dict(nt=2), dict(dst=heap.stride - 512),
+           dict(src=heap.stride + 16), dict(remote=0, dst=off + 512)]
+    for change in bad:
+        a = {**good, **change}
+        with pytest.raises(pkg.SymtileError) as e:
+            pkg.symtile_value_exercise(heap.handle, a["op"], a["src"], a["dst"], a["n"],
+                                       a["cur"], a["remote"], a["nt"], st)
+        assert e.value.name == "EINVAL", change
+    heap.barrier()
 
 
 # ---------------------------------------------------------------- heap tile copy
