@@ -843,10 +843,10 @@ const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
     static const Variant table[] = {
         make_variant<64, 64, false, 4>(),    make_variant<64, 64, true, 4>(),
         make_variant<128, 128, false, 4>(),  make_variant<128, 128, true, 4>(),
+        make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),
         make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
         make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
-        make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 224, false, 8, 16>(), make_variant<256, 224, true, 8, 16>(),
     };
     for (const Variant& v : table)
