@@ -12,12 +12,13 @@
 //     dispatched round-robin over the 8 XCDs, so the tiles in flight on one
 //     XCD are made spatial neighbours) followed by a GROUP_M swizzle
 //     (Section 3.4, swizzling);
-//   * main loop (Section 4, GEMM main-loop listing): 4 waves in a 2 x 2
-//     layout, each owning a (BM/2) x (BN/2) block of 32x32 MFMA
-//     accumulators (v_mfma_f32_32x32x16_{bf16,f16}, fp32 accumulate);
-//     A and B tiles of BK = 64 are staged through LDS, double buffered, with
-//     an XOR swizzle that keeps both the staging writes and the fragment
-//     reads free of bank conflicts.  Both tiles go global -> LDS directly
+//   * main loop (Section 4, GEMM main-loop listing): 8 waves (two per SIMD;
+//     4 for the small tiles), each owning a block of 32x32 MFMA accumulators
+//     (v_mfma_f32_32x32x16_{bf16,f16}, fp32 accumulate; 16x16x32 for the
+//     256x224 tile); A and B stages of BK = 32 go through a 4-stage LDS ring,
+//     loaded 3 stages ahead, with XOR swizzles that keep both the staging
+//     writes and the fragment reads free of bank conflicts.  Both tiles go
+//     global -> LDS directly
 //     (buffer loads into LDS), A as [m][k] rows read with 16-byte LDS reads,
 //     B as [k][n] rows, whose MFMA operands (8 consecutive k of one column)
 //     come from two transposing LDS reads (ds_read_b64_tr_b16);
