@@ -547,13 +547,15 @@ void gas_kernel(const GasParams p) {
                 for (int e = 0; e < ACC_N; ++e) acc[i][j][e] = 0.0f;
 
         // A and B straight into LDS stage `buf`.  A chunks at k >= K read
-        // zero (offset replaced by one outside the resource); B rows at
-        // k >= K lie past the end of B's resource and read zero too.
+        // zero: bit 31 (kOOB) is set in their offset, taken from the sign of
+        // K - 1 - k (arithmetic rather than a select, which would keep the
+        // constant in a vector register), so it lies past the resource; B
+        // rows at k >= K lie past the end of B's resource and read zero too.
         auto load_tile = [&](int kt, int buf) {
             const int k0 = kt * BK;
             uint8_t* As = smem + buf * STAGE;
-            const uint32_t va = (k0 + 8 * a_chunk < p.K) ? a_row_off + a_chunk * 16
-                                                          : symtile::kOOB;
+            const uint32_t va = (a_row_off + a_chunk * 16) |
+                                ((uint32_t)(p.K - 1 - k0 - 8 * a_chunk) & symtile::kOOB);
 #pragma unroll
             for (int u = 0; u < A_INSTR; ++u)
                 symtile::buf_ld16_lds_async(rA, symtile::lds_addr(As + (NW * u + wave) * 1024),
