@@ -90,6 +90,11 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--cpu-configs", action="store_true",
+                    help="also time the oracle on every workload (all host threads, and one "
+                         "thread for the two small ones) and report it as cpu_configs")
+    ap.add_argument("--oracle-time", default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--oracle-rows", type=int, default=0, help=argparse.SUPPRESS)
     ap.add_argument("--calibrate-traffic", action="store_true",
                     help="also run a plain 256 MiB device copy (known bytes) for counter runs")
     return ap.parse_args(argv)
@@ -212,13 +217,92 @@ def bench_copy(args, torch, sym, workload):
     }
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+
+
+def oracle_gemm_rate(wl, rows: int, seconds: float, workload) -> dict:
+    """The oracle (GEMM + placement into every slot + counters) on rows
+    0..rows-1 of A of workload wl, rank 0, repeated for about `seconds`."""
+    import oracle
+    A, B = workload.workload_inputs(wl, 0)
+    Ab, Bb = workload.bits(A), workload.bits(B)
+    st = oracle.GatheredState(wl.world, rows, wl.N_local, wl.tile_m, wl.tile_n)
+    done, total = 0, 0.0
+    while (total < seconds and done < 1000) or done == 0:
+        t0 = time.perf_counter()
+        oracle.gemm_all_scatter(st, Ab[:rows], Bb, wl.dtype, 0)
+        total += time.perf_counter() - t0
+        done += 1
+    flops = 2.0 * rows * wl.N_local * wl.K * done
+    return {"value": flops / total / 1e12, "unit": "TFLOP/s", "cores": oracle_threads(),
+            "rows": rows, "of_rows": wl.M, "repetitions": done, "seconds": round(total, 2)}
+
+
+def oracle_time_child(name: str, rows: int, seconds: float, threads: int) -> dict:
+    """oracle_gemm_rate in a child process with `threads` OpenMP threads (the
+    OpenMP runtime fixes its thread count at start-up).  The child touches no
+    GPU."""
+    import subprocess
+    env = dict(os.environ, OMP_NUM_THREADS=str(threads))
+    out = subprocess.run([sys.executable, os.path.abspath(__file__), "--oracle-time", name,
+                          "--oracle-rows", str(rows), "--cpu-seconds", str(seconds)],
+                         env=env, capture_output=True, text=True, check=True)
+    return json.loads(out.stdout.strip().splitlines()[-1])
+
+
+def cpu_configs(args, workload) -> dict:
+    """The oracle on every GEMM workload (bounded row samples of the large
+    ones) with all host threads, and with one thread on the two small ones."""
+    out = {}
+    secs = max(1.0, args.cpu_seconds / 4)
+    for wl in workload.GEMM_WORKLOADS.values():
+        rows = min(wl.M, 512)
+        out[wl.name] = oracle_gemm_rate(wl, rows, secs, workload)
+    for wl in (workload.TINY, workload.SMALL_BF16):
+        out[wl.name + " (1 thread)"] = oracle_time_child(wl.name, min(wl.M, 512), secs, 1)
+    return out
+
+
+def copy_cpu_baseline(args, workload) -> dict:
+    """The oracle's heap tile copy (one thread) on the whole copy workload."""
+    import numpy as np
+
+    import oracle
+    wl = workload.HEAP_COPY
+    send = workload.copy_send(wl).numpy()
+    recv = np.zeros_like(send)
+    done, total = 0, 0.0
+    while (total < max(1.0, args.cpu_seconds / 4) and done < 100) or done == 0:
+        t0 = time.perf_counter()
+        oracle.tile_copy(send, recv, args.copy_tile, args.copy_tile, shift=wl.shift)
+        total += time.perf_counter() - t0
+        done += 1
+    return {"value": wl.bytes_moved * done / total / 1e9, "unit": "GB/s", "cores": 1,
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": f"the whole workload ({wl.world} x {wl.rows}x{wl.cols} fp32, "
+                      f"{args.copy_tile}x{args.copy_tile} tiles, ring r -> r+{wl.shift}), "
+                      f"{done} calls, {total:.1f} s"}
+
+
 def cpu_baseline(args, wl, A, B, workload):
     """The oracle (GEMM + placement into every slot + counters) timed on the
     host cores on the first rows of the same workload, repeated until about
     --cpu-seconds of work; TFLOP/s."""
     import oracle
     Ab, Bb = workload.bits(A), workload.bits(B)
-    threads = int(os.environ.get("OMP_NUM_THREADS", len(os.sched_getaffinity(0))))
+    threads = oracle_threads()
     rows = min(512, wl.M)                 # bounds the oracle's gathered state (~0.6 GB)
     st = oracle.GatheredState(wl.world, rows, wl.N_local, 256, 256)
     done, total = 0, 0.0
@@ -229,6 +313,7 @@ def cpu_baseline(args, wl, A, B, workload):
         done += 1
     flops = 2.0 * rows * wl.N_local * wl.K * done
     return {"value": flops / total / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"rows 0..{rows - 1} of A (of {wl.M}) against rank 0's shard "
                       f"[{wl.K}, {wl.N_local}]: fp32 GEMM + placement into {wl.world} slots + "
                       f"counters, {done} repetitions, {total:.1f} s"}
@@ -236,6 +321,12 @@ def cpu_baseline(args, wl, A, B, workload):
 
 def main(argv=None):
     args = parse_args(argv)
+    if args.oracle_time:                  # child of oracle_time_child: CPU only
+        import workload
+        wl = workload.GEMM_WORKLOADS[args.oracle_time]
+        print(json.dumps(oracle_gemm_rate(wl, args.oracle_rows or wl.M, args.cpu_seconds,
+                                          workload)), flush=True)
+        return 0
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (the emulated ranks live in one "
               f"GPU's HBM); --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -268,8 +359,12 @@ def main(argv=None):
     }
     if not args.no_copy:
         line["tile_copy"] = bench_copy(args, torch, sym, workload)
+        if not args.no_cpu_baseline:
+            line["tile_copy"]["cpu_baseline"] = copy_cpu_baseline(args, workload)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args, wl, A, B, workload)
+        if args.cpu_configs:
+            line["cpu_configs"] = cpu_configs(args, workload)
     if args.calibrate_traffic:
         # a plain copy kernel of known size: 256 MiB read + 256 MiB written
         x = torch.ones(1 << 28, dtype=torch.uint8, device="cuda")

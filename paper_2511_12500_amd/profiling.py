@@ -3,6 +3,10 @@
 Turns a ``--kernel-trace --stats`` kernel_stats CSV and two ``--pmc`` runs
 (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch) into a short text summary:
 average launch duration of one kernel, and its memory traffic per launch.
+An optional third ``--pmc`` run (GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES,
+SQ_BUSY_CU_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 or _F16) adds the clock the
+kernel ran at, the share of SIMD cycles its matrix cores were busy, and its
+throughput against the matrix-core peak at the spec clock and at that clock.
 The counters are calibrated against a plain device copy of known size that
 ran in the same process (``bench.py --calibrate-traffic``): each counter is
 scaled by known_bytes / counter_value(copy), so the figure is in bytes even
@@ -80,6 +84,66 @@ def counter_per_dispatch(path: str, counter: str, kernel: str) -> tuple[float, i
     return statistics.median(per.values()), len(per), name
 
 
+def dispatch_counters(path: str, kernel: str, last: int = 0) -> tuple[str, list[dict]]:
+    """Per dispatch of the first kernel whose name matches: every counter
+    summed over its instances, and the dispatch's duration in ns (from the
+    counter run's own timestamps).  Dispatch order = dispatch id; with
+    last > 0 only the last `last` dispatches are kept."""
+    rx = re.compile(kernel)
+    per: dict[int, dict] = {}
+    name = ""
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if not rx.search(row["Kernel_Name"]):
+                continue
+            if not name:
+                name = row["Kernel_Name"]
+            if row["Kernel_Name"] != name:
+                continue
+            d = per.setdefault(int(row["Dispatch_Id"]), {
+                "dur_ns": float(row["End_Timestamp"]) - float(row["Start_Timestamp"])})
+            d[row["Counter_Name"]] = d.get(row["Counter_Name"], 0.0) + float(row["Counter_Value"])
+    if not per:
+        raise KeyError(f"no dispatch of kernel {kernel!r} in {path}")
+    rows = [per[k] for k in sorted(per)]
+    return name, rows[-last:] if last else rows
+
+
+def mfma_lines(path: str, kernel: str, last: int, cus: int, xcds: int, flops: float | None,
+               peak_clk_ghz: float, flops_per_clk_cu: float) -> list[str]:
+    """Matrix-core evidence from one --pmc run (medians over dispatches):
+    clock = GRBM_GUI_ACTIVE / xcds / duration (GRBM_GUI_ACTIVE counts GPU
+    clocks once per XCD); MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x
+    cus x clocks); counted flops = SQ_INSTS_VALU_MFMA_MOPS_* x 512."""
+    _, rows = dispatch_counters(path, kernel, last)
+    med = lambda xs: statistics.median(xs)
+    mops = next((c for c in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F16")
+                 if c in rows[0]), None)
+    clk = [r["GRBM_GUI_ACTIVE"] / xcds / r["dur_ns"] for r in rows]      # GHz
+    busy = [r["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * cus * r["GRBM_GUI_ACTIVE"] / xcds) for r in rows]
+    out = ["",
+           f"- clock (GRBM_GUI_ACTIVE / {xcds} XCDs / duration): {med(clk):.3f} GHz "
+           f"(median of {len(rows)} dispatches)",
+           f"- MFMA busy (SQ_VALU_MFMA_BUSY_CYCLES / (4 x {cus} SIMDs x clocks)): "
+           f"{100 * med(busy):.1f}% of all SIMD cycles"]
+    if "SQ_BUSY_CU_CYCLES" in rows[0]:
+        out.append(f"- SQ_BUSY_CU_CYCLES per dispatch: {med([r['SQ_BUSY_CU_CYCLES'] for r in rows]):.0f}")
+    if mops:
+        counted = med([r[mops] for r in rows]) * 512
+        out.append(f"- MFMA flops counted ({mops} x 512): {counted:.4g}"
+                   + (f" (algorithmic {flops:.4g})" if flops else ""))
+    if flops:
+        dur = med([r["dur_ns"] for r in rows])
+        ach = flops / dur / 1e3                                          # TFLOP/s
+        spec = cus * flops_per_clk_cu * peak_clk_ghz / 1e3
+        at_clk = cus * flops_per_clk_cu * med(clk) / 1e3
+        out.append(f"- in this run: {dur:.0f} ns per dispatch, {ach:.1f} TFLOP/s = "
+                   f"{100 * ach / spec:.1f}% of the spec peak ({spec:.0f} TFLOP/s at "
+                   f"{peak_clk_ghz} GHz), {100 * ach / at_clk:.1f}% of the peak at the measured "
+                   f"clock ({at_clk:.0f} TFLOP/s)")
+    return out
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--trace", required=True,
@@ -95,6 +159,13 @@ def main(argv=None) -> int:
     ap.add_argument("--algorithmic-bytes", type=float, default=None)
     ap.add_argument("--sources", nargs="*", default=[])
     ap.add_argument("--command", action="append", default=[])
+    ap.add_argument("--mfma", help="run_counter_collection.csv of the matrix-core --pmc run")
+    ap.add_argument("--flops", type=float, default=None, help="algorithmic flops per dispatch")
+    ap.add_argument("--cus", type=int, default=256)
+    ap.add_argument("--xcds", type=int, default=8)
+    ap.add_argument("--peak-clock-ghz", type=float, default=2.4)
+    ap.add_argument("--flops-per-clk-cu", type=float, default=4096.0,
+                    help="dense bf16/fp16 matrix-core flops per clock per CU")
     ap.add_argument("--title", default="")
     ap.add_argument("--out", required=True)
     a = ap.parse_args(argv)
@@ -122,10 +193,14 @@ def main(argv=None) -> int:
                   f"WRITE_SIZE {cw:.0f} -> scale {f_scale:.2f} / {w_scale:.2f} B per unit",
                   f"- fetch_bytes_per_dispatch: {fetch_b:.0f}",
                   f"- write_bytes_per_dispatch: {write_b:.0f}",
-                  f"- bytes_per_dispatch: {fetch_b + write_b:.0f}"]
+                  f"- bytes_per_dispatch: {fetch_b + write_b:.0f}",
+                  f"- counted bytes / avg duration: {(fetch_b + write_b) / t['avg_ns']:.1f} GB/s"]
         if a.algorithmic_bytes:
             lines.append(f"- algorithmic_bytes_per_dispatch: {a.algorithmic_bytes:.0f} "
                          f"(counters / algorithmic = {(fetch_b + write_b) / a.algorithmic_bytes:.2f})")
+    if a.mfma:
+        lines += mfma_lines(a.mfma, a.kernel, a.last, a.cus, a.xcds, a.flops, a.peak_clock_ghz,
+                            a.flops_per_clk_cu)
     if a.sources:
         lines += ["", f"- source_sha: {sources_sha(a.sources)}  (of: {' '.join(a.sources)})"]
     with open(a.out, "w") as f:

@@ -51,6 +51,7 @@ def test_last_n_dispatches_and_calibrated_bytes(csvs, tmp_path):
     assert "- fetch_bytes_per_dispatch: 240" in text
     assert "- write_bytes_per_dispatch: 10" in text
     assert "- bytes_per_dispatch: 250" in text
+    assert "- counted bytes / avg duration: 1.7 GB/s" in text     # 250 B / 150 ns
     assert f"- source_sha: {profiling.sources_sha([str(src)])}" in text
 
 
@@ -74,3 +75,33 @@ def test_bench_reads_traffic_only_for_matching_sources(tmp_path, monkeypatch):
     src.write_text("v2")                               # kernel changed since the counters
     assert bench.counter_traffic("gas.md", [str(src)]) is None
     assert bench.counter_traffic("absent.md", [str(src)]) is None
+
+
+def test_matrix_core_evidence(tmp_path):
+    k = "void gas_kernel<256, 256, true, 8>(P)"
+    hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+           "End_Timestamp"]
+    rows = []
+    # 2 CUs on 2 XCDs, 1000 ns per dispatch; dispatch 1 is dropped by --last 2.
+    # GRBM_GUI_ACTIVE 4000 over 2 XCDs in 1000 ns = 2.0 GHz (2000 clocks);
+    # MFMA busy 4000 of 4 x 2 x 2000 SIMD cycles = 25%; flops 1e6 in 1000 ns =
+    # 1 TFLOP/s against 2 x 4096 x 2.4 GHz = 19.66 TFLOP/s spec (5.1%) and
+    # 2 x 4096 x 2.0 GHz = 16.38 at the measured clock (6.1%).
+    for d, (grbm, busy) in enumerate([(9999, 1), (4000, 4000), (4000, 4000)]):
+        t0 = 10000 * d
+        for name, val in (("GRBM_GUI_ACTIVE", grbm / 2), ("GRBM_GUI_ACTIVE", grbm / 2),
+                          ("SQ_VALU_MFMA_BUSY_CYCLES", busy), ("SQ_BUSY_CU_CYCLES", 7),
+                          ("SQ_INSTS_VALU_MFMA_MOPS_BF16", 1e6 / 512)):
+            rows.append([d, k, name, val, t0, t0 + 1000])
+    _write(tmp_path / "mfma.csv", hdr, rows)
+    _write(tmp_path / "trace.csv", ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+           [[k, 0, 900], [k, 1000, 1900], [k, 2000, 2900]])
+    out = tmp_path / "m.md"
+    profiling.main(["--trace", str(tmp_path / "trace.csv"), "--last", "2", "--kernel",
+                    "gas_kernel", "--mfma", str(tmp_path / "mfma.csv"), "--flops", "1e6",
+                    "--cus", "2", "--xcds", "2", "--out", str(out)])
+    text = out.read_text()
+    assert "- clock (GRBM_GUI_ACTIVE / 2 XCDs / duration): 2.000 GHz (median of 2 dispatches)" in text
+    assert "25.0% of all SIMD cycles" in text
+    assert "- MFMA flops counted (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): 1e+06 (algorithmic 1e+06)" in text
+    assert "1.0 TFLOP/s = 5.1% of the spec peak (20 TFLOP/s at 2.4 GHz), 6.1% of the peak at the measured clock (16 TFLOP/s)" in text
