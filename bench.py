@@ -78,7 +78,9 @@ def parse_args(argv=None):
     ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
     ap.add_argument("--variant", default="fused_seq",
                     choices=["bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec"])
-    ap.add_argument("--tile", default="256x256")
+    ap.add_argument("--tile", default=None,
+                    help="output tile MxN (default 256x256; 256x128 for wave_spec, the only "
+                         "tile that schedule is built for)")
     ap.add_argument("--gemm-wgs", type=int, default=0)
     ap.add_argument("--copy-wgs", type=int, default=0)
     ap.add_argument("--group-m", type=int, default=0)
@@ -103,6 +105,8 @@ def parse_args(argv=None):
 
 def bench_gas(args, torch, sym, workload):
     wl = workload.GEMM_WORKLOADS[args.workload]
+    if args.tile is None:
+        args.tile = "256x128" if args.variant == "wave_spec" else "256x256"
     tm, tn = (int(x) for x in args.tile.split("x"))
     variant = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
                "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[args.variant]
