@@ -105,3 +105,17 @@ def test_matrix_core_evidence(tmp_path):
     assert "25.0% of all SIMD cycles" in text
     assert "- MFMA flops counted (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): 1e+06 (algorithmic 1e+06)" in text
     assert "1.0 TFLOP/s = 5.1% of the spec peak (20 TFLOP/s at 2.4 GHz), 6.1% of the peak at the measured clock (16 TFLOP/s)" in text
+
+
+def test_bench_refuses_more_than_one_gpu(capsys):
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.main(["--gpus", "2"]) == 2
+    assert "one GPU only" in capsys.readouterr().err
+
+
+def test_bench_default_tile_follows_the_schedule():
+    sys.path.insert(0, ROOT)
+    import bench
+    assert bench.parse_args([]).tile is None            # resolved in bench_gas
+    assert bench.parse_args(["--tile", "128x128"]).tile == "128x128"
