@@ -269,10 +269,11 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
         }
     }
     symtile::wg_stores_done();
-    if (tid == 0) {
+    if (tid < 64) {            // wave 0: one release, then lane d counts slot rank + d
         symtile::release_agent();
         uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
-        for (int d = 1; d < p.world; ++d)
+        const int d = tid + 1;
+        if (d < p.world)
             symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
     }
 }
@@ -370,14 +371,13 @@ __device__ void copy_wave_tiles(const GasParams& p, int KT) {
         };
         auto publish = [&]() {
             __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            if (lane == 0) {
-                symtile::release_agent();
-                uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + ptm) * p.tiles_n + ptn;
-                for (int d = 1; d < p.world; ++d)
-                    symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world,
-                                                         p.bases));
-                if (p.trace) tile_trace(p, ptm, ptn)[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
-            }
+            symtile::release_agent();           // one release; lane d counts slot rank + d
+            uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + ptm) * p.tiles_n + ptn;
+            if (lane >= 1 && lane < p.world)
+                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + lane) % p.world,
+                                                     p.bases));
+            if (lane == 0 && p.trace)
+                tile_trace(p, ptm, ptn)[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
         };
         if (ptm >= 0 && piped) {
             // interval b loads group b (b < GROUPS) and stores group b-2
@@ -773,14 +773,14 @@ void gas_kernel(const GasParams p) {
             }
         }
         symtile::wg_stores_done();     // also orders the LDS reads above before reuse
-        if (tid == 0) {
-            if (p.trace) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
+        if (tid < 64) {                // wave 0: one release, then lane d counts slot rank + d
+            if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
             symtile::release_agent();
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
-            for (int d = 0; d < n_dst; ++d)
-                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
-            if (p.role == ROLE_WG_SPEC) symtile::flag_add(p.ready + tm * p.tiles_n + tn);
-            if (p.trace) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
+            if (tid < n_dst)
+                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + tid) % p.world, p.bases));
+            if (tid == 0 && p.role == ROLE_WG_SPEC) symtile::flag_add(p.ready + tm * p.tiles_n + tn);
+            if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
         }
     }
 }

@@ -209,11 +209,13 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
         }
     }
     // Publish: every tile of the run is in its destination heap before any
-    // of its counters moves.
+    // of its counters moves.  Wave 0 releases once, then its lanes increment
+    // the run's counters together (one tile per lane), rather than one
+    // thread issuing them one after another into the same cache lines.
     symtile::wg_stores_done();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < 64) {
         symtile::release_agent();
-        for (int it = first; it < last; ++it) {
+        for (int it = first + (int)threadIdx.x; it < last; it += 64) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
             int src, dst;
             copy_ranks(p, r, src, dst);
