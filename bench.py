@@ -67,6 +67,21 @@ def counter_traffic(name: str, sources) -> float | None:
         return None
 
 
+def gas_profile_name(args, wl) -> str:
+    """The profiles/ summary that holds the counters of exactly this launch
+    configuration (workload, schedule, tile, store policy, split)."""
+    if (args.variant, args.tile, args.nontemporal, args.gemm_wgs, args.copy_wgs,
+            args.group_m) == ("fused_seq", "256x256", 2, 0, 0, 0):
+        return f"gas_kernel_{wl.name}.md"
+    return (f"gas_kernel_{wl.name}_{args.variant}_{args.tile}_nt{args.nontemporal}"
+            f"_g{args.gemm_wgs}_c{args.copy_wgs}_m{args.group_m}.md")
+
+
+def copy_profile_name(args, wl) -> str:
+    name = f"tile_copy_kernel_{wl.name}_t{args.copy_tile}"
+    return name + (f"_per{args.copy_per_wg}" if args.copy_per_wg else "") + ".md"
+
+
 def parse_args(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,7 +162,7 @@ def bench_gas(args, torch, sym, workload):
     kernel_s = ms_per_step * 1e-3
     achieved = flops / kernel_s / 1e12
     peak = PEAK_MFMA_TFLOPS[wl.dtype]
-    traffic = counter_traffic(f"gas_kernel_{wl.name}.md", KERNEL_SOURCES)
+    traffic = counter_traffic(gas_profile_name(args, wl), KERNEL_SOURCES)
     res = {
         "value": flops / (ms_per_step * 1e-3) / 1e12,
         "ms_per_step": ms_per_step,
@@ -213,7 +228,7 @@ def bench_copy(args, torch, sym, workload):
     cold_mean_ms = statistics.fmean(cold)
     warm_ms = sum(warm) / len(warm)
     gbs = moved / (cold_ms * 1e-3) / 1e9
-    traffic = counter_traffic(f"tile_copy_kernel_{wl.name}_t{t}.md", COPY_SOURCES)
+    traffic = counter_traffic(copy_profile_name(args, wl), COPY_SOURCES)
     heap.close()
     del flush
     return {

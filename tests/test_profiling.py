@@ -119,3 +119,19 @@ def test_bench_default_tile_follows_the_schedule():
     import bench
     assert bench.parse_args([]).tile is None            # resolved in bench_gas
     assert bench.parse_args(["--tile", "128x128"]).tile == "128x128"
+
+
+def test_bench_profile_names_are_per_configuration():
+    sys.path.insert(0, ROOT)
+    import bench
+    import workload
+    wl = workload.LARGE_BF16
+    a = bench.parse_args([])
+    a.tile = "256x256"
+    assert bench.gas_profile_name(a, wl) == f"gas_kernel_{wl.name}.md"
+    b = bench.parse_args(["--variant", "wg_spec", "--gemm-wgs", "224", "--copy-wgs", "32"])
+    b.tile = "256x256"
+    assert bench.gas_profile_name(b, wl) == \
+        f"gas_kernel_{wl.name}_wg_spec_256x256_nt2_g224_c32_m0.md"
+    assert bench.copy_profile_name(a, workload.HEAP_COPY) == \
+        f"tile_copy_kernel_{workload.HEAP_COPY.name}_t128.md"
