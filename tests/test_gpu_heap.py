@@ -248,7 +248,7 @@ def _copy_heap(pkg, world, rows, cols, dtype_t):
 
 
 @pytest.mark.parametrize("mode", [0, 1], ids=["put", "get"])
-@pytest.mark.parametrize("tile,per_wg", [(64, 0), (128, 0), (256, 0), (128, 1), (64, 7)])
+@pytest.mark.parametrize("tile,per_wg", [(64, 0), (128, 0), (256, 0), (128, 1), (64, 7), (64, 96)])
 def test_heap_tile_copy_workload_bitexact(tile, per_wg, mode):
     """All 8 ranks copy send -> recv of rank (r+1) mod 8, 2048 x 2048 fp32
     (put: each rank writes the next rank's heap; get: each rank reads the
