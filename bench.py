@@ -69,12 +69,14 @@ def counter_traffic(name: str, sources) -> float | None:
 
 def gas_profile_name(args, wl) -> str:
     """The profiles/ summary that holds the counters of exactly this launch
-    configuration (workload, schedule, tile, store policy, split)."""
+    configuration (workload, schedule, tile, store policy, producer/consumer
+    split, K slices)."""
+    sk = f"_k{args.split_k}" if args.split_k > 1 else ""
     if (args.variant, args.tile, args.nontemporal, args.gemm_wgs, args.copy_wgs,
-            args.group_m) == ("fused_seq", "256x256", 2, 0, 0, 0):
+            args.group_m, sk) == ("fused_seq", "256x256", 2, 0, 0, 0, ""):
         return f"gas_kernel_{wl.name}.md"
     return (f"gas_kernel_{wl.name}_{args.variant}_{args.tile}_nt{args.nontemporal}"
-            f"_g{args.gemm_wgs}_c{args.copy_wgs}_m{args.group_m}.md")
+            f"_g{args.gemm_wgs}_c{args.copy_wgs}_m{args.group_m}{sk}.md")
 
 
 def copy_profile_name(args, wl) -> str:
@@ -99,6 +101,8 @@ def parse_args(argv=None):
     ap.add_argument("--gemm-wgs", type=int, default=0)
     ap.add_argument("--copy-wgs", type=int, default=0)
     ap.add_argument("--group-m", type=int, default=0)
+    ap.add_argument("--split-k", type=int, default=0,
+                    help="K slices per output tile (bulk_sync, fused_seq; 0 or 1 = none)")
     ap.add_argument("--nontemporal", type=int, default=2,
                     help="output store policy: 0 default, 1 non-temporal, 2 write-through")
     ap.add_argument("--copy-tile", type=int, default=128)
@@ -132,7 +136,7 @@ def bench_gas(args, torch, sym, workload):
     heap = sym.Heap(wl.world, slot)
     out = sym.GatheredOutput(heap, wl.M, wl.N_local, workload.torch_dtype(wl.dtype), tm, tn)
     kw = dict(gemm_wgs=args.gemm_wgs, copy_wgs=args.copy_wgs, nontemporal=args.nontemporal,
-              group_m=args.group_m)
+              group_m=args.group_m, split_k=args.split_k)
 
     def step():
         out.run(dA, dB, 0, variant, **kw)
@@ -174,7 +178,8 @@ def bench_gas(args, torch, sym, workload):
         "config": {"workload": wl.name, "M": wl.M, "K": wl.K, "N_local": wl.N_local,
                    "world_size": wl.world, "rank": 0, "N_gathered": wl.N_gathered,
                    "variant": args.variant, "tile": args.tile, "gemm_wgs": args.gemm_wgs,
-                   "copy_wgs": args.copy_wgs, "nontemporal": args.nontemporal},
+                   "copy_wgs": args.copy_wgs, "nontemporal": args.nontemporal,
+                   "split_k": max(args.split_k, 1)},
         "dtype": wl.dtype,
     }
     heap.close()

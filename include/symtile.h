@@ -90,7 +90,27 @@ typedef struct {
     uint64_t* trace;      /* optional per-tile timeline (Section 3.4, instrumentation):
                              device uint64 [tiles_m*tiles_n][SYMTILE_TRACE_WORDS],
                              tile (m, n) at row m*tiles_n + n; NULL = off.  See
-                             symtile_trace_word for the layout. */
+                             symtile_trace_word for the layout.  With split_k > 1
+                             the start, location and main-loop words are those of
+                             the tile's first K slice, the stored and released
+                             words those of the slice that reduces the tile. */
+    int split_k;          /* BULK_SYNC and FUSED_SEQ: each output tile is computed
+                             as split_k slices of K (0 or 1 = no split; at most
+                             64 and at most ceil(K/32)), so a problem with fewer
+                             tiles than CUs still fills the chip.  The slices of
+                             a tile add their fp32 partial products in slice
+                             order, whichever finishes last, so the result is
+                             the same on every call (it differs from split_k = 1
+                             only by fp32 rounding). */
+    void* workspace;      /* split_k > 1: device memory of workspace_bytes >=
+                             symtile_gas_workspace_bytes(...) bytes, 16-byte
+                             aligned, outside the output and counters.  Its first
+                             round_up(8 * tiles, 256) bytes are counters that must
+                             be zero before the first call that uses it; every
+                             call leaves them zero again (after an ETIMEOUT, zero
+                             them again).  Calls that share a workspace must not
+                             overlap in time (same stream, or synchronised). */
+    size_t workspace_bytes;
 } symtile_gas_config;
 
 /* Per-tile trace record.  Times are ticks of the device's constant-rate
@@ -260,6 +280,15 @@ symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off
 
 /* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
 
+/* Bytes of the split-K workspace (symtile_gas_config.workspace) of a call
+ * with this output shape, tile and split_k: two uint32 counters per tile
+ * (rounded up to 256 bytes), then split_k fp32 partial tiles of
+ * tile_m * tile_n values per tile.  *bytes = 0 when split_k <= 1.  EINVAL for
+ * negative sizes, a tile shape that is not built (see tile_m, tile_n above)
+ * or split_k > 64. */
+symtile_status symtile_gas_workspace_bytes(int M, int N_local, int tile_m, int tile_n,
+                                           int split_k, size_t* bytes);
+
 /* Rank `rank`'s share: C_r = A * B_shard with an fp32 accumulator (Section 4
  * GEMM main loop), rounded to the input dtype (nearest even), stored into the
  * rank's column block [rank*N_local, (rank+1)*N_local) of the gathered output
@@ -288,7 +317,12 @@ symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off
  * stores zeros).  WG_SPEC requires gemm_wgs + copy_wgs workgroups to be
  * co-resident (checked; EUNSUPPORTED otherwise).  A consumer wait that
  * exceeds cfg->spin_limit polls records ETIMEOUT for the next
- * symtile_barrier, and that consumer abandons its remaining tiles. */
+ * symtile_barrier, and that consumer abandons its remaining tiles.  With
+ * split_k > 1 the slice that finishes a tile last waits (bounded by
+ * cfg->spin_limit) only for slices that have already started; a timeout
+ * records ETIMEOUT and leaves that tile unwritten and unpublished.  split_k > 1
+ * with another variant is EUNSUPPORTED; without a large enough workspace, or
+ * with split_k above ceil(K/32), EINVAL. */
 symtile_status symtile_gemm_all_scatter(symtile_heap* h, const void* A, const void* B_shard,
                                         void* C_gathered_local, uint32_t* arrived_local,
                                         uint32_t* ready, int M, int N_local, int K, int lda,

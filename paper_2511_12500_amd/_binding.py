@@ -43,6 +43,9 @@ class GasConfig(ctypes.Structure):
         ("waves_per_wg", ctypes.c_int),
         ("copy_stream", ctypes.c_void_p),
         ("trace", ctypes.c_void_p),
+        ("split_k", ctypes.c_int),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
     ]
 
 
@@ -76,6 +79,7 @@ def _load():
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "symtile_gas_workspace_bytes": [i32, i32, i32, i32, i32, ctypes.POINTER(sz)],
         "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
         "symtile_litmus_mp": [vp, sz, sz, i32, i32, i32, i32, u32, vp, vp],
         "symtile_value_exercise": [vp, i32, sz, sz, sz, i32, i32, i32, vp],
@@ -219,6 +223,15 @@ def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int
                                         dtype, rank, world_size,
                                         ctypes.byref(cfg) if cfg is not None else None,
                                         _vp(stream)), "symtile_gemm_all_scatter")
+
+
+def symtile_gas_workspace_bytes(M: int, N_local: int, tile_m: int, tile_n: int,
+                                split_k: int) -> int:
+    """Bytes of the split-K workspace of a call (0 when split_k <= 1)."""
+    out = ctypes.c_size_t()
+    _check(lib.symtile_gas_workspace_bytes(M, N_local, tile_m, tile_n, split_k, ctypes.byref(out)),
+           "symtile_gas_workspace_bytes")
+    return out.value
 
 
 def symtile_litmus_mp(h: int, data_off: int, flag_off: int, pairs: int, rounds: int,

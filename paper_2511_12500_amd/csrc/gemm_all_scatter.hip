@@ -80,6 +80,11 @@ struct GasParams {
     uint32_t epoch, spin_limit;
     int nontemporal;
     uint64_t* trace;        // [num_tiles][8] per-tile timeline, or nullptr
+    // Split-K: each tile is `split` work units, unit s covering stages
+    // [s*KT/split, (s+1)*KT/split) of the KT stages of K; units = tiles * split.
+    int split, units;
+    uint32_t* sk_cnt;       // [num_tiles][2]: arrival ticket, partials written
+    float* sk_part;         // [num_tiles][split][BM*BN] fp32 partial tiles
 };
 
 // Trace record of tile (tm, tn), or nullptr when tracing is off.
@@ -150,13 +155,23 @@ __device__ __forceinline__ int swz_b(int k) {
     return lo ^ (((k >> 3) & 1) << 1);
 }
 
-// Producer-order tile index t -> (tile row, tile column).
-__device__ __forceinline__ void tile_coords(int t, int G, const GasParams& p, int& tm, int& tn) {
-    int L = t;
-    const int round = t / G;
-    if ((G & 7) == 0 && (round + 1) * G <= p.num_tiles) {
-        const int pos = t - round * G;
+// Producer-order work unit u -> (tile row, tile column, K slice).  The XCD
+// remap makes consecutive units land on one XCD, and the slices of a tile are
+// consecutive units, so with split-K they share that XCD's L2 (and the
+// partial tiles they exchange stay there).  Without split-K a unit is a tile.
+__device__ __forceinline__ void unit_coords(int u, int G, const GasParams& p, int& tm, int& tn,
+                                            int& s) {
+    int L = u;
+    const int round = u / G;
+    if ((G & 7) == 0 && (round + 1) * G <= p.units) {
+        const int pos = u - round * G;
         L = round * G + (pos & 7) * (G >> 3) + (pos >> 3);
+    }
+    if (p.split > 1) {
+        s = L % p.split;
+        L /= p.split;
+    } else {
+        s = 0;
     }
     const int width = p.group_m * p.tiles_n;
     const int group = L / width;
@@ -165,6 +180,13 @@ __device__ __forceinline__ void tile_coords(int t, int G, const GasParams& p, in
     const int in = L - group * width;
     tm = first_m + in % gsize;
     tn = in / gsize;
+}
+
+// Producer-order tile index t -> (tile row, tile column), for schedules
+// without split-K (units == tiles).
+__device__ __forceinline__ void tile_coords(int t, int G, const GasParams& p, int& tm, int& tn) {
+    int s;
+    unit_coords(t, G, p, tm, tn, s);
 }
 
 template <bool BF16>
@@ -481,13 +503,13 @@ void gas_kernel(const GasParams p) {
 
     // ---------------- producer workgroups ---------------------------------
     const int G = p.gemm_wgs;
-    const int KT = (p.K + BK - 1) / BK;
+    const int KT_all = (p.K + BK - 1) / BK;    // stages of the whole K
     if constexpr (CW) {
         // the copy wave (Section 4.2.3); the test is made visibly uniform so
         // that the compiler keeps the copy wave's addressing scalar
         if (__builtin_amdgcn_readfirstlane(wave) == NW) {
             with_store_policy(p.nontemporal, [&](auto pol) {
-                copy_wave_tiles<BM, BN, decltype(pol)::value>(p, KT);
+                copy_wave_tiles<BM, BN, decltype(pol)::value>(p, KT_all);
             });
             return;
         }
@@ -521,22 +543,29 @@ void gas_kernel(const GasParams p) {
     const int tr_row = ((MF == 32) ? 8 * (lane >> 5) : 8 * (lane >> 4)) + ((lane & 15) >> 2);
     const int tr_col = ((MF == 32) ? 16 * ((lane >> 4) & 1) : 0) + 4 * (lane & 3);
 
-    for (int t = pid; t < p.num_tiles; t += G) {
-        int tm, tn;
-        tile_coords(t, G, p, tm, tn);
+    for (int t = pid; t < p.units; t += G) {
+        int tm, tn, ks;
+        unit_coords(t, G, p, tm, tn, ks);
+        // this unit's K slice: stages [kt0, kt0 + KT)
+        const int kt0 = ks * KT_all / p.split;
+        const int KT = (ks + 1) * KT_all / p.split - kt0;
         // (the trace record's address is recomputed at each event so that
         // nothing extra stays live across the K loop)
-        if (p.trace && tid == 0) {
+        if (p.trace && tid == 0 && ks == 0) {
             uint64_t* tr = tile_trace(p, tm, tn);
             tr[SYMTILE_TRACE_START] = symtile::clock_now();
             tr[SYMTILE_TRACE_WHERE] = symtile::trace_location();
         }
         const int m0 = tm * BM, n0 = tn * BN;
         const int rows_a = min(BM, p.M - m0);
+        // The resources start at the slice's first k, so the loop indexes
+        // stages from 0 and sees kend = the K left from there.
+        const int kbeg = kt0 * BK, kend = p.K - kbeg;
         const symtile::i32x4_t rA = symtile::make_rsrc_words(
-            p.A + (size_t)m0 * p.lda, (uint32_t)(rows_a * p.lda * 2));
+            p.A + (size_t)m0 * p.lda + kbeg, (uint32_t)(rows_a * p.lda * 2 - kbeg * 2));
         const symtile::i32x4_t rB = symtile::make_rsrc_words(
-            p.B + n0, p.K > 0 ? (uint32_t)((size_t)p.K * p.ldb * 2 - (size_t)n0 * 2) : 0u);
+            p.B + (size_t)kbeg * p.ldb + n0,
+            kend > 0 ? (uint32_t)((size_t)kend * p.ldb * 2 - (size_t)n0 * 2) : 0u);
 
         acc_t acc[MI][NI];
 #pragma unroll
@@ -546,16 +575,17 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int e = 0; e < ACC_N; ++e) acc[i][j][e] = 0.0f;
 
-        // A and B straight into LDS stage `buf`.  A chunks at k >= K read
-        // zero: bit 31 (kOOB) is set in their offset, taken from the sign of
-        // K - 1 - k (arithmetic rather than a select, which would keep the
-        // constant in a vector register), so it lies past the resource; B
-        // rows at k >= K lie past the end of B's resource and read zero too.
+        // A and B straight into LDS stage `buf` (k relative to the slice).
+        // A chunks at k >= K read zero: bit 31 (kOOB) is set in their offset,
+        // taken from the sign of K - 1 - k (arithmetic rather than a select,
+        // which would keep the constant in a vector register), so it lies
+        // past the resource; B rows at k >= K lie past the end of B's
+        // resource and read zero too.
         auto load_tile = [&](int kt, int buf) {
             const int k0 = kt * BK;
             uint8_t* As = smem + buf * STAGE;
             const uint32_t va = (a_row_off + a_chunk * 16) |
-                                ((uint32_t)(p.K - 1 - k0 - 8 * a_chunk) & symtile::kOOB);
+                                ((uint32_t)(kend - 1 - k0 - 8 * a_chunk) & symtile::kOOB);
 #pragma unroll
             for (int u = 0; u < A_INSTR; ++u)
                 symtile::buf_ld16_lds_async(rA, symtile::lds_addr(As + (NW * u + wave) * 1024),
@@ -717,7 +747,114 @@ void gas_kernel(const GasParams p) {
             mfmas1();              // last stage, group 1
         }
         __syncthreads();           // every wave is done with the ring
-        if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
+        if (p.trace && tid == 0 && ks == 0)
+            tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
+
+        // ---- split-K: combine the K slices of the tile ------------------
+        // Every slice takes an arrival ticket.  A slice that is not the last
+        // to arrive writes its fp32 partial tile, releases it and counts it
+        // as written, and moves on.  The last one waits until the others'
+        // partials are written: they all took their tickets before it, so
+        // they are running and wait for nothing themselves (no deadlock, and
+        // no co-residency is assumed).  It then acquires them and forms the
+        // sum in slice order, so the result does not depend on which slice
+        // came last, and goes on to the epilogue with the tile's full sum.
+        if (p.split > 1) {
+            __shared__ uint32_t s_ticket, s_ok;
+            const int tile = tm * p.tiles_n + tn;
+            uint32_t* cnt = p.sk_cnt + 2 * tile;
+            if (tid == 0)
+                s_ticket = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
+            __syncthreads();
+            const bool last = __builtin_amdgcn_readfirstlane(s_ticket) + 1 == (uint32_t)p.split;
+            // Partial tile of slice q: each thread's accumulators, 16 bytes
+            // per (i, j, 4-value group), so a wave's access is 1 KiB contiguous.
+            auto slot = [&](int q) {
+                return symtile::make_rsrc(p.sk_part + ((size_t)tile * p.split + q) * (BM * BN),
+                                          (uint32_t)(BM * BN * 4));
+            };
+            auto put_partial = [&](int q) {
+                const symtile::rsrc_t rs = slot(q);
+#pragma unroll
+                for (int i = 0; i < MI; ++i)
+#pragma unroll
+                    for (int j = 0; j < NI; ++j)
+#pragma unroll
+                        for (int g = 0; g < ACC_N / 4; ++g) {
+                            // (element copies first: this compiler's bit_cast of
+                            // a vector element reads the vector's element 0)
+                            const f32x4_t f{acc[i][j][4 * g], acc[i][j][4 * g + 1],
+                                            acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+                            const symtile::u32x4 v = __builtin_bit_cast(symtile::u32x4, f);
+                            symtile::buf_st16p<symtile::kStoreWriteThrough>(
+                                v, rs, (uint32_t)tid * 16,
+                                (uint32_t)(((i * NI + j) * (ACC_N / 4) + g) * THREADS * 16));
+                        }
+            };
+            // acc = partial q (first) or acc + partial q, in batches of 8
+            // loads (32 registers): scheduling fences keep the compiler from
+            // hoisting every load at once, which would need 4 registers per
+            // accumulator register.
+            auto add_partial = [&](int q, bool first) {
+                const symtile::rsrc_t rs = slot(q);
+                constexpr int GPA = ACC_N / 4;                 // 4-value groups per accumulator
+                constexpr int NG = MI * NI * GPA;
+                constexpr int BATCH = NG % 8 == 0 ? 8 : NG % 4 == 0 ? 4 : 1;
+                static_assert(NG % BATCH == 0, "batch split");
+#pragma unroll
+                for (int b = 0; b < NG; b += BATCH) {
+                    symtile::u32x4 v[BATCH];
+#pragma unroll
+                    for (int x = 0; x < BATCH; ++x)
+                        v[x] = symtile::buf_ld16(rs, (uint32_t)tid * 16,
+                                                 (uint32_t)((b + x) * THREADS * 16));
+#pragma unroll
+                    for (int x = 0; x < BATCH; ++x) {
+                        const int n = b + x, i = n / (NI * GPA), j = (n / GPA) % NI, g = n % GPA;
+                        const f32x4_t y = __builtin_bit_cast(f32x4_t, v[x]);   // whole vector
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            acc[i][j][4 * g + e] = first ? y[e] : acc[i][j][4 * g + e] + y[e];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            };
+            if (!last) {
+                put_partial(ks);
+                symtile::wg_stores_done();
+                if (tid == 0) {
+                    symtile::release_agent();
+                    symtile::flag_add(cnt + 1);
+                }
+                continue;
+            }
+            if (tid == 0) {
+                const bool ok = symtile::flag_wait_geq(cnt + 1, (uint32_t)p.split - 1, p.spin_limit);
+                if (ok)
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                else
+                    symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+                // every slice of this call has counted itself: the next call
+                // starts again from zero
+                symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
+                symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                s_ok = ok;
+            }
+            __syncthreads();
+            if (!s_ok) continue;
+            // Two slices: acc + the other partial, which is p0 + p1 either
+            // way (fp32 addition commutes).  More: this slice's partial joins
+            // the others in memory and the sum is formed p0 + p1 + ... in
+            // slice order.  (One call site of add_partial: with two, the
+            // compiler spills inside the K loop.)
+            if (p.split > 2) {
+                put_partial(ks);
+                __builtin_amdgcn_s_waitcnt(vm_wait(0));
+            }
+            const int nq = p.split == 2 ? 1 : p.split;
+            for (int n = 0; n < nq; ++n)
+                add_partial(p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
+        }
 
         // ---- epilogue: round, restage row-major, store, release --------
         uint8_t* Cs = smem;
@@ -877,7 +1014,28 @@ symtile_status coresident_limit(const Variant* v, int device, int* cus, int* lim
     return SYMTILE_OK;
 }
 
+// Split-K workspace: two counters per tile, rounded up to 256 bytes, then
+// `split` fp32 partial tiles per tile.
+constexpr int kMaxSplit = 64;
+size_t sk_counter_bytes(size_t tiles) { return (tiles * 8 + 255) / 256 * 256; }
+size_t sk_workspace_bytes(size_t tiles, int bm, int bn, int split) {
+    return split <= 1 ? 0 : sk_counter_bytes(tiles) + tiles * split * (size_t)bm * bn * 4;
+}
+
 }  // namespace
+
+extern "C" symtile_status symtile_gas_workspace_bytes(int M, int N_local, int tile_m, int tile_n,
+                                                      int split_k, size_t* bytes) {
+    using symtile_host::fail;
+    if (!bytes) return fail(SYMTILE_EINVAL, "bytes is NULL");
+    if (M < 0 || N_local < 0) return fail(SYMTILE_EINVAL, "negative size");
+    if (tile_m == 0 && tile_n == 0) tile_m = tile_n = 256;
+    if (!find_variant(tile_m, tile_n, true, 0)) return fail(SYMTILE_EINVAL, "tile shape not built");
+    if (split_k < 0 || split_k > kMaxSplit) return fail(SYMTILE_EINVAL, "split_k must be 0..64");
+    const size_t tiles = (size_t)((M + tile_m - 1) / tile_m) * ((N_local + tile_n - 1) / tile_n);
+    *bytes = sk_workspace_bytes(tiles, tile_m, tile_n, split_k);
+    return SYMTILE_OK;
+}
 
 extern "C" symtile_status symtile_device_info(int device, int tile_m, int tile_n, int* cu_count,
                                               int* max_coresident_wgs) {
@@ -917,6 +1075,10 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         return fail(SYMTILE_EINVAL, "K, N_local, lda and ldb must be multiples of 8");
     if (cfg.waves_per_wg != 0 && cfg.waves_per_wg != 4 && cfg.waves_per_wg != 8)
         return fail(SYMTILE_EINVAL, "waves_per_wg must be 0, 4 or 8");
+    if (cfg.split_k < 0 || cfg.split_k > kMaxSplit) return fail(SYMTILE_EINVAL, "split_k must be 0..64");
+    const int split = cfg.split_k > 1 ? cfg.split_k : 1;
+    if (split > 1 && cfg.variant != SYMTILE_FUSED_SEQ && cfg.variant != SYMTILE_BULK_SYNC)
+        return fail(SYMTILE_EUNSUPPORTED, "split_k > 1 is built for BULK_SYNC and FUSED_SEQ");
     const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16, cfg.waves_per_wg);
     if (!v) return fail(SYMTILE_EUNSUPPORTED, "tile shape / wave count not built");
     // Buffer resources span one tile row band of A or C and the whole of B;
@@ -953,6 +1115,27 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         return fail(SYMTILE_EINVAL, "WG_SPEC and UNFUSED_PC need a ready counter array");
     if (reinterpret_cast<uintptr_t>(cfg.trace) % 8)
         return fail(SYMTILE_EINVAL, "trace must be 8-byte aligned");
+    if (split > 1) {
+        if (split > (K + BK - 1) / BK)
+            return fail(SYMTILE_EINVAL, "split_k " + std::to_string(split) +
+                                            " exceeds the ceil(K/32) stages of K");
+        if (num_tiles * split > (size_t)INT32_MAX) return fail(SYMTILE_EINVAL, "too many work units");
+        const size_t need = sk_workspace_bytes(num_tiles, cfg.tile_m, cfg.tile_n, split);
+        if (!cfg.workspace || cfg.workspace_bytes < need)
+            return fail(SYMTILE_EINVAL, "split_k needs a workspace of " + std::to_string(need) +
+                                            " bytes");
+        if (reinterpret_cast<uintptr_t>(cfg.workspace) % 16)
+            return fail(SYMTILE_EINVAL, "workspace must be 16-byte aligned");
+        const uint64_t w0 = reinterpret_cast<uint64_t>(cfg.workspace);
+        const uint64_t c0 = reinterpret_cast<uint64_t>(C_gathered_local);
+        const uint64_t f0 = reinterpret_cast<uint64_t>(arrived_local);
+        for (int s = 0; s < world_size; ++s) {   // the output and counters of every slot
+            const uint64_t cs = c0 + (uint64_t)s * h->slot_stride - (uint64_t)rank * h->slot_stride;
+            const uint64_t fs = f0 + (uint64_t)s * h->slot_stride - (uint64_t)rank * h->slot_stride;
+            if ((w0 < cs + c_bytes && cs < w0 + need) || (w0 < fs + flag_bytes && fs < w0 + need))
+                return fail(SYMTILE_EINVAL, "workspace overlaps the output or the counters");
+        }
+    }
 
     int cus = 0, limit = 0;
     if (symtile_status st = coresident_limit(v, h->device, &cus, &limit)) return st;
@@ -984,6 +1167,12 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         return fail(SYMTILE_EINVAL, "nontemporal must be 0, 1 or 2");
     p.trace = cfg.trace;
     p.copy_wgs = 0;
+    p.split = split;
+    p.units = (int)(num_tiles * split);
+    p.sk_cnt = split > 1 ? static_cast<uint32_t*>(cfg.workspace) : nullptr;
+    p.sk_part = split > 1 ? reinterpret_cast<float*>(static_cast<uint8_t*>(cfg.workspace) +
+                                                     sk_counter_bytes(num_tiles))
+                          : nullptr;
 
     hipStream_t stream = static_cast<hipStream_t>(s);
     int prev = -1;
@@ -997,8 +1186,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
 
     const int ntiles = (int)num_tiles;
     if (cfg.variant == SYMTILE_FUSED_SEQ || cfg.variant == SYMTILE_BULK_SYNC) {
-        int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : std::min(ntiles, cus);
-        g = std::min(g, ntiles);
+        int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : std::min(p.units, cus);
+        g = std::min(g, p.units);
         p.gemm_wgs = g;
         p.role = cfg.variant == SYMTILE_FUSED_SEQ ? ROLE_FUSED : ROLE_LOCAL_ONLY;
         void* args[] = {&p};

@@ -113,6 +113,7 @@ class GatheredOutput:
         self.ready = torch.zeros(max(self.tiles_m * self.tiles_n, 1), dtype=torch.int32,
                                  device=heap.mem.device)
         self.ready_epoch = 0     # value of every ready counter after the last WG_SPEC call
+        self.ws = None           # split-K workspace (uint8 device tensor), grown on demand
 
     def C(self, rank: int) -> torch.Tensor:
         return self.heap.view(rank, self.c_off, (self.M, self.heap.world * self.N_local),
@@ -130,6 +131,19 @@ class GatheredOutput:
         return self.heap.slots_view(self.flag_off, (self.heap.world, self.tiles_m, self.tiles_n),
                                     torch.int32)
 
+    def workspace(self, split_k: int) -> torch.Tensor | None:
+        """The split-K workspace for ``split_k`` slices (None when split_k <= 1):
+        a zeroed uint8 device tensor, kept and reused by later calls (each call
+        leaves its counters at zero), replaced by a larger one when needed."""
+        need = B.symtile_gas_workspace_bytes(self.M, self.N_local, self.tile_m, self.tile_n,
+                                             split_k)
+        if need == 0:
+            return None
+        if self.ws is None or self.ws.numel() < need:
+            self.ws = None
+            self.ws = torch.zeros(need, dtype=torch.uint8, device=self.heap.mem.device)
+        return self.ws
+
     def new_trace(self) -> torch.Tensor:
         """Zeroed per-tile trace buffer [tiles_m * tiles_n, 8] (int64, on the
         heap's device); tile (m, n) is row m * tiles_n + n."""
@@ -140,13 +154,16 @@ class GatheredOutput:
             gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
             spin_limit: int = 0, epoch: int | None = None, stream: int | None = None,
             waves_per_wg: int = 0, trace: torch.Tensor | None = None,
-            copy_stream: int | None = None) -> None:
+            copy_stream: int | None = None, split_k: int = 0) -> None:
         """One call of rank ``rank`` (enqueued on the stream, asynchronous).
         For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
         more than after the previous WG_SPEC call on these buffers.
         ``trace``: optional int64 device tensor from new_trace(), filled with
         the per-tile timeline of this call.  ``copy_stream``: UNFUSED_PC's
-        copy-kernel stream (default: one the heap creates)."""
+        copy-kernel stream (default: one the heap creates).  ``split_k`` > 1
+        (BULK_SYNC, FUSED_SEQ): each tile is computed as that many K slices,
+        with this object's workspace; calls on one object that use split-K
+        must not overlap in time."""
         if A.dtype != self.dtype or B_shard.dtype != self.dtype:
             raise TypeError("A and B_shard must have the output dtype")
         if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):
@@ -166,6 +183,11 @@ class GatheredOutput:
                           spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
                           waves_per_wg=waves_per_wg, copy_stream=copy_stream,
                           trace=trace.data_ptr() if trace is not None else None)
+        if split_k > 1:
+            ws = self.workspace(split_k)
+            cfg.split_k, cfg.workspace, cfg.workspace_bytes = split_k, ws.data_ptr(), ws.numel()
+        elif split_k:
+            cfg.split_k = split_k
         dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
         B.symtile_gemm_all_scatter(
             self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),

@@ -97,3 +97,48 @@ def test_build_module_imports_without_the_library(tmp_path):
     r = subprocess.run([sys.executable, "-c", code], cwd=tmp_path, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
     assert "raised" in r.stdout and "not built" in r.stdout
+
+
+def test_gas_config_mirror_matches_the_header(tmp_path):
+    """The binding's GasConfig has the size and field offsets of
+    symtile_gas_config as a C compiler lays it out from the header."""
+    import shutil
+    import subprocess
+    from paper_2511_12500_amd._binding import GasConfig
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    names = [f[0] for f in GasConfig._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include <stdio.h>\n#include <stddef.h>\n#include "symtile.h"\nint main(void) {\n'
+        '  printf("size %zu\\n", sizeof(symtile_gas_config));\n' +
+        "".join(f'  printf("{n} %zu\\n", offsetof(symtile_gas_config, {n}));\n' for n in names) +
+        "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                        check=True).stdout.splitlines())
+    assert int(out["size"]) == ctypes.sizeof(GasConfig)
+    for n in names:
+        assert int(out[n]) == getattr(GasConfig, n).offset, n
+
+
+def test_split_k_workspace_size_is_host_only(libpath):
+    """Two uint32 counters per tile rounded up to 256 bytes, then split_k fp32
+    partial tiles per tile; 0 without a split; argument errors."""
+    import paper_2511_12500_amd as pkg
+    ws = pkg.symtile_gas_workspace_bytes
+    assert ws(8192, 1024, 256, 256, 2) == 1024 + 128 * 2 * 256 * 256 * 4
+    assert ws(1024, 1024, 256, 256, 16) == 256 + 16 * 16 * 256 * 256 * 4
+    assert ws(300, 136, 128, 128, 3) == 256 + 6 * 3 * 128 * 128 * 4
+    assert ws(3000, 3000, 64, 64, 2) == (47 * 47 * 8 + 255) // 256 * 256 + 47 * 47 * 2 * 64 * 64 * 4
+    assert ws(4096, 3584, 256, 224, 2) == 2048 + 256 * 2 * 256 * 224 * 4
+    for split in (0, 1):
+        assert ws(8192, 1024, 256, 256, split) == 0
+    assert ws(0, 1024, 256, 256, 2) == 0                   # no tiles: nothing to keep
+    for bad in ((8192, 1024, 256, 256, 65), (8192, 1024, 256, 256, -1),
+                (8192, 1024, 32, 32, 2), (-1, 1024, 256, 256, 2)):
+        with pytest.raises(pkg.SymtileError) as e:
+            ws(*bad)
+        assert e.value.name == "EINVAL", bad

@@ -494,3 +494,153 @@ def test_wave_spec_other_tiles_unsupported():
         p.run(0, WAVESPEC)
     assert e.value.name == "EUNSUPPORTED"
     p.heap.barrier()
+
+
+# ---------------------------------------------------------------- split-K
+
+SPLITK = [
+    # world, M, N_local, K, tile_m, tile_n, dtype, split_k
+    (2, 300, 136, 520, 128, 128, "bf16", 2),     # ragged M, N; 17 stages split 8 + 9
+    (3, 257, 264, 1000, 256, 256, "f16", 3),     # 32 stages 10/11/11, last stage 8 of 32 k
+    (4, 130, 264, 72, 256, 128, "bf16", 3),      # one stage per slice, the last ragged
+    (5, 77, 40, 200, 64, 64, "f16", 7),          # one stage per slice, 7 slices
+    (8, 64, 8, 64, 64, 64, "bf16", 2),           # one tile, 8 columns
+    (3, 300, 504, 200, 256, 224, "bf16", 2),     # 16x16x32 MFMA tile shape
+    (2, 512, 512, 2048, 256, 256, "bf16", 8),    # 8 slices of 8 stages
+]
+
+
+def _ws_counters(p):
+    n = 2 * p.out.tiles_m * p.out.tiles_n
+    return p.out.ws[:n * 4].view(torch.int32).cpu().numpy()
+
+
+@pytest.mark.parametrize("case", SPLITK, ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_s%d" % c)
+@pytest.mark.parametrize("variant", [FUSED, BULK], ids=VNAMES.get)
+def test_split_k_all_ranks(case, variant):
+    """Each tile as split_k slices of K: placement and counters bit-exact,
+    values within tolerance, and the workspace counters back at zero."""
+    world, M, N, K, tm, tn, dtype, split = case
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=11)
+    want = _blocks(p)
+    p.sentinel()
+    for i, r in enumerate(reversed(range(world))):
+        p.run(r, variant, split_k=split)
+        if i == 0:
+            p.barrier()
+            check_gathered(p, want)
+            assert np.all(_ws_counters(p) == 0)
+    p.barrier()
+    check_gathered(p, want)
+    assert np.all(_ws_counters(p) == 0)
+
+
+@pytest.mark.parametrize("split", [2, 3, 5])
+def test_split_k_is_deterministic_across_grids(split):
+    """The slices add their partials in slice order, so neither the grid size
+    (how many slices run at once, and which finishes last) nor a repeated
+    call changes a bit."""
+    world, rank = 4, 2
+    p = Problem(world, 520, 392, 1544, "bf16", 128, 128, seed=12)
+    want = {rank: oracle_block(p.A, p.shards[rank], "bf16")}
+    units = p.out.tiles_m * p.out.tiles_n * split
+    ref = None
+    for g in (0, units, 7, 1, 0):
+        p.sentinel()
+        p.run(rank, FUSED, split_k=split, gemm_wgs=g)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[rank]))
+        got = u16(p.out.C_all())
+        if ref is None:
+            ref = got.copy()
+        assert np.array_equal(got, ref), g
+        assert np.all(_ws_counters(p) == 0)
+
+
+def test_split_k_two_slices_match_one_within_rounding():
+    """split_k = 2 changes only the fp32 summation order: against the
+    unsplit call, at most a rounding step of the output in any element."""
+    world, rank = 2, 0
+    p = Problem(world, 512, 256, 4096, "bf16", 256, 256, seed=13, dist="normal_sqrtk")
+    p.sentinel()
+    p.run(rank, FUSED)
+    p.barrier()
+    one = p.out.C(0)[:, :256].float().cpu()
+    p.run(rank, FUSED, split_k=2)
+    p.barrier()
+    two = p.out.C(0)[:, :256].float().cpu()
+    # one bf16 step of the larger value, plus the fp32 reordering error near
+    # zero (about sqrt(K) * 2^-24 * |C|, far below this floor)
+    step = torch.maximum(one.abs(), two.abs()) * 2.0 ** -7 + one.abs().max() * 2.0 ** -16
+    assert bool((torch.abs(one - two) <= step).all())
+    check_block(u16(p.out.C(0)[:, :256]), oracle_block(p.A, p.shards[0], "bf16"), "bf16")
+
+
+@pytest.mark.parametrize("wl", [workload.WIDE_F16, workload.SMALL_BF16], ids=lambda w: w.name)
+def test_split_k_full_size_matches_oracle(wl):
+    """The full-size shapes with few 256x256 tiles (128 and 16), split so
+    every CU has a slice, in the configuration the benchmark runs."""
+    split = 2 if wl is workload.WIDE_F16 else 16
+    p = _large_case(wl, seed=4)
+    want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
+    p.sentinel()
+    p.run(0, FUSED, split_k=split, nontemporal=2)
+    p.barrier()
+    check_gathered(p, want, flag_count=1)
+    assert np.all(_ws_counters(p) == 0)
+
+
+def test_split_k_trace_is_causal():
+    """With split-K the start and main-loop words are slice 0's and the
+    stored and released words the reducing slice's; still in order."""
+    from paper_2511_12500_amd import trace as T
+    world, rank = 4, 1
+    p = Problem(world, 600, 520, 264, "bf16", 128, 128, seed=7)
+    want = {rank: oracle_block(p.A, p.shards[rank], "bf16")}
+    tr = p.out.new_trace()
+    p.sentinel()
+    p.run(rank, FUSED, trace=tr, split_k=3)
+    p.barrier()
+    check_gathered(p, want)
+    raw = tr.cpu().numpy().view(np.uint64)
+    prod = raw[:, [T.START, T.MAINLOOP, T.STORED, T.RELEASED]]
+    assert np.all(prod > 0)
+    assert np.all(np.diff(prod.astype(np.int64), axis=1) >= 0)
+
+
+def test_split_k_argument_errors():
+    pkg = sym()
+    p = Problem(2, 128, 64, 256, "bf16", 64, 64)
+    h = p.heap.handle
+    c0, f0 = p.heap.ptr(0, p.out.c_off), p.heap.ptr(0, p.out.flag_off)
+    ws = p.out.workspace(2)
+    need = pkg.symtile_gas_workspace_bytes(128, 64, 64, 64, 2)
+    assert ws.numel() == need == 256 + 2 * 2 * 64 * 64 * 4       # 2 tiles of 64x64
+
+    def call(**kw):
+        base = dict(variant=FUSED, tile_m=64, tile_n=64, split_k=2, workspace=ws.data_ptr(),
+                    workspace_bytes=need)
+        base.update(kw)
+        K = base.pop("K", 256)
+        pkg.symtile_gemm_all_scatter(h, p.dA.data_ptr(), p.dB[0].data_ptr(), c0, f0,
+                                     p.out.ready.data_ptr(), 128, 64, K, 256, 64, pkg.BF16, 0, 2,
+                                     pkg.GasConfig(**base), 0)
+
+    for kw, name in ((dict(variant=WGSPEC, gemm_wgs=8, copy_wgs=8), "EUNSUPPORTED"),
+                     (dict(variant=UNFUSED), "EUNSUPPORTED"),
+                     (dict(variant=WAVESPEC), "EUNSUPPORTED"),
+                     (dict(split_k=65), "EINVAL"),
+                     (dict(split_k=-1), "EINVAL"),
+                     (dict(split_k=9), "EINVAL"),                   # K = 256 has 8 stages
+                     (dict(workspace=None), "EINVAL"),
+                     (dict(workspace_bytes=need - 1), "EINVAL"),
+                     (dict(workspace=ws.data_ptr() + 8), "EINVAL"),  # misaligned
+                     (dict(workspace=c0, workspace_bytes=1 << 20), "EINVAL")):   # overlaps C
+        with pytest.raises(pkg.SymtileError) as e:
+            call(**kw)
+        assert e.value.name == name, kw
+    p.sentinel()
+    p.run(0, FUSED, split_k=8)                                        # 8 stages: allowed
+    p.barrier()
+    check_gathered(p, {0: oracle_block(p.A, p.shards[0], "bf16")})
+    assert np.all(_ws_counters(p) == 0)

@@ -135,3 +135,10 @@ def test_bench_profile_names_are_per_configuration():
         f"gas_kernel_{wl.name}_wg_spec_256x256_nt2_g224_c32_m0.md"
     assert bench.copy_profile_name(a, workload.HEAP_COPY) == \
         f"tile_copy_kernel_{workload.HEAP_COPY.name}_t128.md"
+    c = bench.parse_args(["--workload", workload.WIDE_F16.name, "--split-k", "2"])
+    c.tile = "256x256"
+    assert bench.gas_profile_name(c, workload.WIDE_F16) == \
+        f"gas_kernel_{workload.WIDE_F16.name}_fused_seq_256x256_nt2_g0_c0_m0_k2.md"
+    d = bench.parse_args(["--split-k", "1"])
+    d.tile = "256x256"
+    assert bench.gas_profile_name(d, wl) == f"gas_kernel_{wl.name}.md"
