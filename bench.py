@@ -15,7 +15,6 @@ HBM peak, and the CPU oracle timed on a bounded sample as a baseline.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import statistics
@@ -37,11 +36,9 @@ COPY_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", f)
 
 
 def sources_sha(paths) -> str:
-    h = hashlib.sha256()
-    for p in paths:
-        with open(p, "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+    """The profiles' hash of the kernel code (comments and layout ignored)."""
+    from paper_2511_12500_amd.profiling import sources_sha as sha
+    return sha(paths)
 
 
 def counter_traffic(name: str, sources) -> float | None:

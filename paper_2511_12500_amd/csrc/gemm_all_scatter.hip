@@ -33,6 +33,11 @@
 //     and put the tile into the other w-1 heaps (pointer-based put).
 //   * bulk-synchronous (Section 4.1.1): producers store locally, and a
 //     second kernel on the same stream puts every tile to the other heaps.
+//   * split-K (an addition to the paper's schedules, for shapes with fewer
+//     tiles than CUs): with split > 1 a work unit is one K slice of a tile;
+//     the slices meet through fp32 partial tiles in a caller workspace, and
+//     the last slice to arrive sums them in slice order and runs the
+//     epilogue above.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

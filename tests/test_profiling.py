@@ -77,6 +77,19 @@ def test_bench_reads_traffic_only_for_matching_sources(tmp_path, monkeypatch):
     assert bench.counter_traffic("absent.md", [str(src)]) is None
 
 
+def test_source_hash_ignores_comments_and_layout(tmp_path):
+    """A comment or whitespace edit keeps the profiles valid; a code edit does not."""
+    sys.path.insert(0, ROOT)
+    from paper_2511_12500_amd import profiling
+    src = tmp_path / "k.hip"
+    src.write_text("int f(int x) {\n    return x + 1;   // one more\n}\n")
+    h = profiling.sources_sha([str(src)])
+    src.write_text("/* header\n   comment */\nint f(int x)\n{\n  return x + 1; // changed note\n}\n")
+    assert profiling.sources_sha([str(src)]) == h
+    src.write_text("int f(int x) {\n    return x + 2;\n}\n")
+    assert profiling.sources_sha([str(src)]) != h
+
+
 def test_matrix_core_evidence(tmp_path):
     k = "void gas_kernel<256, 256, true, 8>(P)"
     hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
