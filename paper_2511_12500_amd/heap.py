@@ -183,11 +183,10 @@ class GatheredOutput:
                           spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
                           waves_per_wg=waves_per_wg, copy_stream=copy_stream,
                           trace=trace.data_ptr() if trace is not None else None)
-        if split_k > 1:
-            ws = self.workspace(split_k)
-            cfg.split_k, cfg.workspace, cfg.workspace_bytes = split_k, ws.data_ptr(), ws.numel()
-        elif split_k:
-            cfg.split_k = split_k
+        cfg.split_k = split_k
+        ws = self.workspace(split_k) if split_k > 1 else None
+        if ws is not None:               # None: no tiles, nothing to keep
+            cfg.workspace, cfg.workspace_bytes = ws.data_ptr(), ws.numel()
         dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
         B.symtile_gemm_all_scatter(
             self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),

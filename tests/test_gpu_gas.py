@@ -154,7 +154,23 @@ def test_empty_problem_is_a_noop():
     B = torch.zeros(64, 64, dtype=torch.float16, device="cuda")
     for v in VARIANTS:
         out.run(A, B, 0, v)
+    out.run(A, B, 0, FUSED, split_k=2)          # no tiles: no workspace needed
     heap.barrier()
+
+
+def test_k_zero_with_split_k():
+    """K = 0 has no stage to split: split_k > 1 is refused, split_k = 1 stores zeros."""
+    pkg = sym()
+    p = Problem(2, 64, 64, 0, "bf16", 64, 64, A=torch.zeros(64, 0, dtype=torch.bfloat16),
+                shards=[torch.zeros(0, 64, dtype=torch.bfloat16)] * 2)
+    p.sentinel()
+    with pytest.raises(pkg.SymtileError) as e:
+        p.out.run(p.dA, p.dB[0], 0, FUSED, split_k=2)
+    assert e.value.name == "EINVAL"
+    p.run(0, FUSED, split_k=1)
+    p.barrier()
+    G = u16(p.out.C_all())
+    assert np.all(G[:, :, :64] == 0) and np.all(G[:, :, 64:] == SENTINEL)
 
 
 # ---------------------------------------------------------------- evaluation workloads
