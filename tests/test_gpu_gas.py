@@ -660,3 +660,46 @@ def test_split_k_argument_errors():
     p.barrier()
     check_gathered(p, {0: oracle_block(p.A, p.shards[0], "bf16")})
     assert np.all(_ws_counters(p) == 0)
+
+
+# ---------------------------------------------------------------- seeded random sweep
+
+def _random_cases(n=64, seed=2027):
+    """Seeded draws over world size, shape (ragged M, N, K), tile, wave count,
+    schedule, split-K, dtype and rank; each is a valid call."""
+    rng = np.random.RandomState(seed)
+    tiles = [(64, 64), (128, 128), (256, 128), (256, 256), (256, 224)]
+    cases = []
+    for _ in range(n):
+        world = int(rng.randint(1, 9))
+        tm, tn = tiles[rng.randint(len(tiles))]
+        M = int(rng.randint(1, 700))
+        N = 8 * int(rng.randint(1, 76))
+        K = 8 * int(rng.randint(1, 151))
+        dtype = ("bf16", "f16")[rng.randint(2)]
+        variants = [BULK, FUSED, WGSPEC, UNFUSED] + ([WAVESPEC] if (tm, tn) == (256, 128) else [])
+        variant = variants[rng.randint(len(variants))]
+        waves = 0
+        if (tm, tn) in ((256, 128), (256, 256)) and variant != WAVESPEC and rng.rand() < 0.3:
+            waves = 4
+        split = 0
+        stages = -(-K // 32)
+        if variant in (BULK, FUSED) and stages > 1 and rng.rand() < 0.5:
+            split = min(stages, (2, 2, 3, 4, 6)[rng.randint(5)])
+        rank = int(rng.randint(world))
+        cases.append((world, M, N, K, tm, tn, dtype, variant, waves, split, rank))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_cases(),
+                         ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_v%d_wv%d_s%d_r%d" % c)
+def test_random_calls_match_oracle(case):
+    world, M, N, K, tm, tn, dtype, variant, waves, split, rank = case
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=M + N + K)
+    want = {rank: oracle_block(p.A, p.shards[rank], dtype)}
+    p.sentinel()
+    p.run(rank, variant, waves_per_wg=waves, split_k=split)
+    p.barrier()
+    check_gathered(p, want)
+    if split > 1:
+        assert np.all(_ws_counters(p) == 0)
