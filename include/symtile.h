@@ -67,9 +67,10 @@ typedef struct {
     int variant;          /* symtile_variant */
     int tile_m, tile_n;   /* output tile; (64,64) (128,128) (256,128) (256,256)
                              (256,224); 0,0 = 256x256 */
-    int gemm_wgs;         /* producer workgroups; 0 = min(tiles, CU count) for
-                             BULK_SYNC/FUSED_SEQ, CU count - copy_wgs for WG_SPEC
-                             and UNFUSED_PC */
+    int gemm_wgs;         /* producer workgroups; 0 = min(work units, CU count) for
+                             BULK_SYNC/FUSED_SEQ (a unit is a tile, or one K slice
+                             of a tile with split_k > 1), CU count - copy_wgs for
+                             WG_SPEC and UNFUSED_PC */
     int copy_wgs;         /* WG_SPEC and UNFUSED_PC consumers (0 = CU count / 8) and
                              BULK_SYNC scatter-kernel workgroups (0 = CU count) */
     uint32_t epoch;       /* WG_SPEC, UNFUSED_PC: consumers wait until
@@ -285,7 +286,7 @@ symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off
  * (rounded up to 256 bytes), then split_k fp32 partial tiles of
  * tile_m * tile_n values per tile.  *bytes = 0 when split_k <= 1.  EINVAL for
  * negative sizes, a tile shape that is not built (see tile_m, tile_n above)
- * or split_k > 64. */
+ * or split_k outside 0..64. */
 symtile_status symtile_gas_workspace_bytes(int M, int N_local, int tile_m, int tile_n,
                                            int split_k, size_t* bytes);
 
