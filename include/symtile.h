@@ -84,7 +84,7 @@ typedef struct {
                              line for the release to write back) */
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
-                             (8 for 256x256, 256x224 and 256x128, 4 otherwise) */
+                             (8 for 128x128 and the 256-row tiles, 4 for 64x64) */
     symtile_stream copy_stream; /* UNFUSED_PC: stream of the copy kernel; NULL = a
                              stream the heap creates on first use.  It must not
                              be the call's stream. */

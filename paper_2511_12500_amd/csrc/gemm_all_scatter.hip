@@ -13,7 +13,7 @@
 //     XCD are made spatial neighbours) followed by a GROUP_M swizzle
 //     (Section 3.4, swizzling);
 //   * main loop (Section 4, GEMM main-loop listing): 8 waves (two per SIMD;
-//     4 for the small tiles), each owning a block of 32x32 MFMA accumulators
+//     4 for 64x64 tiles), each owning a block of 32x32 MFMA accumulators
 //     (v_mfma_f32_32x32x16_{bf16,f16}, fp32 accumulate; 16x16x32 for the
 //     256x224 tile); A and B stages of BK = 32 go through a 4-stage LDS ring,
 //     loaded 3 stages ahead, with XOR swizzles that keep both the staging
@@ -987,6 +987,7 @@ Variant make_variant() {
 const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
     static const Variant table[] = {
         make_variant<64, 64, false, 4>(),    make_variant<64, 64, true, 4>(),
+        make_variant<128, 128, false, 8>(),  make_variant<128, 128, true, 8>(),
         make_variant<128, 128, false, 4>(),  make_variant<128, 128, true, 4>(),
         make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),

@@ -389,7 +389,9 @@ def test_argument_errors():
 
 @pytest.mark.parametrize("case", [(8, 1024, 1024, 4096, 256, 256, "bf16"),
                                   (3, 300, 264, 200, 256, 256, "f16"),
-                                  (2, 512, 256, 320, 256, 128, "bf16")],
+                                  (2, 512, 256, 320, 256, 128, "bf16"),
+                                  (4, 300, 264, 200, 128, 128, "bf16"),
+                                  (8, 1024, 1024, 4096, 128, 128, "f16")],
                          ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s" % c)
 def test_four_and_eight_wave_kernels_agree_bitwise(case):
     """Both wave layouts compute each accumulator in the same order, so the
