@@ -130,11 +130,17 @@ def mfma_lines(path: str, kernel: str, last: int, cus: int, xcds: int, flops: fl
                  if c in rows[0]), None)
     clk = [r["GRBM_GUI_ACTIVE"] / xcds / r["dur_ns"] for r in rows]      # GHz
     busy = [r["SQ_VALU_MFMA_BUSY_CYCLES"] / (4 * cus * r["GRBM_GUI_ACTIVE"] / xcds) for r in rows]
+    # Above the peak clock the counter window must be longer than the
+    # dispatch (it happens for dispatches of a few tens of microseconds): the
+    # clock is then unknown and the busy share is a lower bound.
+    window_ok = med(clk) <= peak_clk_ghz * 1.02
     out = ["",
            f"- clock (GRBM_GUI_ACTIVE / {xcds} XCDs / duration): {med(clk):.3f} GHz "
-           f"(median of {len(rows)} dispatches)",
+           f"(median of {len(rows)} dispatches)"
+           + ("" if window_ok else f"; above the {peak_clk_ghz} GHz maximum, so the counter "
+              "window is longer than this short dispatch and the clock is not measured"),
            f"- MFMA busy (SQ_VALU_MFMA_BUSY_CYCLES / (4 x {cus} SIMDs x clocks)): "
-           f"{100 * med(busy):.1f}% of all SIMD cycles"]
+           f"{100 * med(busy):.1f}% of all SIMD cycles" + ("" if window_ok else " (a lower bound)")]
     if "SQ_BUSY_CU_CYCLES" in rows[0]:
         out.append(f"- SQ_BUSY_CU_CYCLES per dispatch: {med([r['SQ_BUSY_CU_CYCLES'] for r in rows]):.0f}")
     if mops:
@@ -146,10 +152,13 @@ def mfma_lines(path: str, kernel: str, last: int, cus: int, xcds: int, flops: fl
         ach = flops / dur / 1e3                                          # TFLOP/s
         spec = cus * flops_per_clk_cu * peak_clk_ghz / 1e3
         at_clk = cus * flops_per_clk_cu * med(clk) / 1e3
-        out.append(f"- in this run: {dur:.0f} ns per dispatch, {ach:.1f} TFLOP/s = "
-                   f"{100 * ach / spec:.1f}% of the spec peak ({spec:.0f} TFLOP/s at "
-                   f"{peak_clk_ghz} GHz), {100 * ach / at_clk:.1f}% of the peak at the measured "
-                   f"clock ({at_clk:.0f} TFLOP/s)")
+        line = (f"- in this run: {dur:.0f} ns per dispatch, {ach:.1f} TFLOP/s = "
+                f"{100 * ach / spec:.1f}% of the spec peak ({spec:.0f} TFLOP/s at "
+                f"{peak_clk_ghz} GHz)")
+        if window_ok:
+            line += (f", {100 * ach / at_clk:.1f}% of the peak at the measured "
+                     f"clock ({at_clk:.0f} TFLOP/s)")
+        out.append(line)
     return out
 
 

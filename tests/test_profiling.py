@@ -118,6 +118,31 @@ def test_matrix_core_evidence(tmp_path):
     assert "25.0% of all SIMD cycles" in text
     assert "- MFMA flops counted (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512): 1e+06 (algorithmic 1e+06)" in text
     assert "1.0 TFLOP/s = 5.1% of the spec peak (20 TFLOP/s at 2.4 GHz), 6.1% of the peak at the measured clock (16 TFLOP/s)" in text
+    assert "not measured" not in text and "lower bound" not in text
+
+
+def test_matrix_core_evidence_flags_a_counter_window_longer_than_the_dispatch(tmp_path):
+    """GRBM_GUI_ACTIVE over the dispatch duration above the peak clock means
+    the counters cover more than the dispatch: no clock, busy share a bound."""
+    k = "void gas_kernel<128, 128, true, 8>(P)"
+    hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+           "End_Timestamp"]
+    rows = []
+    for d in range(2):                 # 6000 clocks over 2 XCDs in 1000 ns = 3.0 GHz
+        for name, val in (("GRBM_GUI_ACTIVE", 3000), ("GRBM_GUI_ACTIVE", 3000),
+                          ("SQ_VALU_MFMA_BUSY_CYCLES", 1200), ("SQ_INSTS_VALU_MFMA_MOPS_BF16", 1e6 / 512)):
+            rows.append([d, k, name, val, 10000 * d, 10000 * d + 1000])
+    _write(tmp_path / "mfma.csv", hdr, rows)
+    _write(tmp_path / "trace.csv", ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+           [[k, 0, 1000], [k, 2000, 3000]])
+    out = tmp_path / "m.md"
+    profiling.main(["--trace", str(tmp_path / "trace.csv"), "--last", "2", "--kernel",
+                    "gas_kernel", "--mfma", str(tmp_path / "mfma.csv"), "--flops", "1e6",
+                    "--cus", "2", "--xcds", "2", "--out", str(out)])
+    text = out.read_text()
+    assert "3.000 GHz" in text and "the clock is not measured" in text
+    assert "(a lower bound)" in text
+    assert "of the spec peak (20 TFLOP/s at 2.4 GHz)" in text and "measured clock (" not in text
 
 
 def test_bench_refuses_more_than_one_gpu(capsys):
