@@ -163,12 +163,14 @@ def bench_gas(args, torch, sym, workload):
     kernel_s = ms_per_step * 1e-3
     achieved = flops / kernel_s / 1e12
     peak = PEAK_MFMA_TFLOPS[wl.dtype]
-    traffic = counter_traffic(gas_profile_name(args, wl), KERNEL_SOURCES)
+    prof = gas_profile_name(args, wl)
+    traffic = counter_traffic(prof, KERNEL_SOURCES)
     res = {
         "value": flops / (ms_per_step * 1e-3) / 1e12,
         "ms_per_step": ms_per_step,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic,
+                     "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
                      "kernel": "gas_kernel<%d,%d,%s>" % (tm, tn, wl.dtype),
                      "algorithmic_flops_per_launch": flops,
                      "avg_launch_ms": kernel_s * 1e3},
@@ -230,7 +232,8 @@ def bench_copy(args, torch, sym, workload):
     cold_mean_ms = statistics.fmean(cold)
     warm_ms = sum(warm) / len(warm)
     gbs = moved / (cold_ms * 1e-3) / 1e9
-    traffic = counter_traffic(copy_profile_name(args, wl), COPY_SOURCES)
+    prof = copy_profile_name(args, wl)
+    traffic = counter_traffic(prof, COPY_SOURCES)
     heap.close()
     del flush
     return {
@@ -241,6 +244,7 @@ def bench_copy(args, torch, sym, workload):
         "warm_GBps": moved / (warm_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": gbs / PEAK_HBM_GBS, "traffic": traffic,
+                     "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
                      "kernel": "tile_copy_kernel", "avg_launch_ms": cold_ms},
     }
 
