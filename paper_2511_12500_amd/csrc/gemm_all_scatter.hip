@@ -764,7 +764,9 @@ void gas_kernel(const GasParams p) {
         // no co-residency is assumed).  It then acquires them and forms the
         // sum in slice order, so the result does not depend on which slice
         // came last, and goes on to the epilogue with the tile's full sum.
-        if (p.split > 1) {
+        // (not built into the copy-wave kernel: wave specialisation has no
+        // split-K, and its third wave per SIMD leaves no registers for it)
+        if (!CW && p.split > 1) {
             __shared__ uint32_t s_ticket, s_ok;
             const int tile = tm * p.tiles_n + tn;
             uint32_t* cnt = p.sk_cnt + 2 * tile;
@@ -796,11 +798,11 @@ void gas_kernel(const GasParams p) {
                                 (uint32_t)(((i * NI + j) * (ACC_N / 4) + g) * THREADS * 16));
                         }
             };
-            // acc = partial q (first) or acc + partial q, in batches of 8
+            // dst = partial q (first) or dst + partial q, in batches of 8
             // loads (32 registers): scheduling fences keep the compiler from
             // hoisting every load at once, which would need 4 registers per
             // accumulator register.
-            auto add_partial = [&](int q, bool first) {
+            auto add_partial = [&](acc_t (&dst)[MI][NI], int q, bool first) {
                 const symtile::rsrc_t rs = slot(q);
                 constexpr int GPA = ACC_N / 4;                 // 4-value groups per accumulator
                 constexpr int NG = MI * NI * GPA;
@@ -819,7 +821,7 @@ void gas_kernel(const GasParams p) {
                         const f32x4_t y = __builtin_bit_cast(f32x4_t, v[x]);   // whole vector
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            acc[i][j][4 * g + e] = first ? y[e] : acc[i][j][4 * g + e] + y[e];
+                            dst[i][j][4 * g + e] = first ? y[e] : dst[i][j][4 * g + e] + y[e];
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -847,18 +849,36 @@ void gas_kernel(const GasParams p) {
             }
             __syncthreads();
             if (!s_ok) continue;
-            // Two slices: acc + the other partial, which is p0 + p1 either
-            // way (fp32 addition commutes).  More: this slice's partial joins
-            // the others in memory and the sum is formed p0 + p1 + ... in
-            // slice order.  (One call site of add_partial: with two, the
-            // compiler spills inside the K loop.)
-            if (p.split > 2) {
-                put_partial(ks);
-                __builtin_amdgcn_s_waitcnt(vm_wait(0));
+            if constexpr (MI * NI * ACC_N <= 64) {
+                // Small accumulators fold in registers:
+                // tmp = p0 + ... + p(ks-1), acc = tmp + acc, which is
+                // (p0 + ... + p(ks-1)) + p(ks) since addition commutes, then
+                // acc += p(ks+1), ... in slice order.
+                acc_t tmp[MI][NI];
+                for (int q = 0; q < ks; ++q) add_partial(tmp, q, q == 0);
+                if (ks > 0) {
+#pragma unroll
+                    for (int i = 0; i < MI; ++i)
+#pragma unroll
+                        for (int j = 0; j < NI; ++j)
+#pragma unroll
+                            for (int e = 0; e < ACC_N; ++e) acc[i][j][e] = tmp[i][j][e] + acc[i][j][e];
+                }
+                for (int q = ks + 1; q < p.split; ++q) add_partial(acc, q, false);
+            } else {
+                // Two slices: acc + the other partial, which is p0 + p1 either
+                // way (fp32 addition commutes).  More: this slice's partial
+                // joins the others in memory and the sum is formed
+                // p0 + p1 + ... in slice order.  (One call site of add_partial:
+                // with two, the compiler spills inside the K loop.)
+                if (p.split > 2) {
+                    put_partial(ks);
+                    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+                }
+                const int nq = p.split == 2 ? 1 : p.split;
+                for (int n = 0; n < nq; ++n)
+                    add_partial(acc, p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
             }
-            const int nq = p.split == 2 ? 1 : p.split;
-            for (int n = 0; n < nq; ++n)
-                add_partial(p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
         }
 
         // ---- epilogue: round, restage row-major, store, release --------
