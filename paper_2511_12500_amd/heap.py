@@ -144,6 +144,12 @@ class GatheredOutput:
             self.ws = torch.zeros(need, dtype=torch.uint8, device=self.heap.mem.device)
         return self.ws
 
+    def reset_workspace(self) -> None:
+        """Zero the split-K workspace (its counters are left non-zero only by a
+        call whose wait timed out, reported as ETIMEOUT by the heap barrier)."""
+        if self.ws is not None:
+            self.ws.zero_()
+
     def new_trace(self) -> torch.Tensor:
         """Zeroed per-tile trace buffer [tiles_m * tiles_n, 8] (int64, on the
         heap's device); tile (m, n) is row m * tiles_n + n."""

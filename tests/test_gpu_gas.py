@@ -657,6 +657,7 @@ def test_split_k_argument_errors():
         with pytest.raises(pkg.SymtileError) as e:
             call(**kw)
         assert e.value.name == name, kw
+    p.out.reset_workspace()
     p.sentinel()
     p.run(0, FUSED, split_k=8)                                        # 8 stages: allowed
     p.barrier()
