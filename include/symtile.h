@@ -38,7 +38,7 @@ typedef enum {
 
 typedef enum { SYMTILE_F16 = 1, SYMTILE_BF16 = 2, SYMTILE_F32 = 3 } symtile_dtype;
 
-/* The three schedules of Section 4 built here. */
+/* The schedules of Section 4 built here. */
 typedef enum {
     SYMTILE_BULK_SYNC = 0,   /* Section 4.1.1: GEMM kernel, then scatter kernel, one stream */
     SYMTILE_FUSED_SEQ = 1,   /* Section 4.2.1: each tile stored to every rank after its K loop */
