@@ -10,7 +10,19 @@ every tile into all 8 slots, per-tile counters.  Inputs are synthetic
 Printed: one JSON line with the GEMM + All-Scatter throughput (TFLOP/s),
 its roofline fraction against the dense bf16 MFMA peak, the heap tile copy
 (2048 x 2048 fp32 per rank, 8 ranks, ring r -> r+1) in GB/s against the
-HBM peak, and the CPU oracle timed on a bounded sample as a baseline.
+HBM peak, and the CPU oracle timed on a bounded sample as a baseline.  The
+``configs`` array adds every other workload and schedule (the tiny fp16
+case, bf16 1024x4096.4096x1024, the schedules and the producer/consumer
+split sweep of the largest shape, the bulk-synchronous / fused /
+specialised comparison on fp16 8192x8192.8192x1024, and the copy with
+64x64 and 256x256 tiles), each with its own roofline fraction, and
+``cpu_configs`` the oracle on every GEMM workload.
+
+Every timed leg first runs a clock-settling phase: the GPU's clocks ramp
+up over roughly the first 100 launches (30 ms) of sustained load after
+idle, so each leg launches its own kernel back to back for at least 100
+launches and 100 ms (reported as ``settle``) before its --warmup launches
+and its timed steps.  --steps and --warmup are used exactly as given.
 """
 from __future__ import annotations
 
@@ -29,10 +41,11 @@ METRIC = "fused GEMM+scatter TFLOP/s (% MFMA peak); heap tile-copy GB/s (% HBM p
 PEAK_MFMA_TFLOPS = {"bf16": 2500.0, "f16": 2500.0}     # MI355X dense bf16/fp16
 PEAK_HBM_GBS = 8000.0                                   # MI355X HBM3E
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", f)
-                  for f in ("gemm_all_scatter.hip", "symtile_device.h")]
-COPY_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", f)
-                for f in ("tile_copy.hip", "symtile_device.h")]
+DEVICE_HEADER = os.path.join(ROOT, "include", "symtile_device.h")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", "gemm_all_scatter.hip"),
+                  DEVICE_HEADER]
+COPY_SOURCES = [os.path.join(ROOT, "paper_2511_12500_amd", "csrc", "tile_copy.hip"),
+                DEVICE_HEADER]
 
 
 def sources_sha(paths) -> str:
@@ -76,19 +89,25 @@ def gas_profile_name(args, wl) -> str:
             f"_g{args.gemm_wgs}_c{args.copy_wgs}_m{args.group_m}{sk}.md")
 
 
-def copy_profile_name(args, wl) -> str:
-    name = f"tile_copy_kernel_{wl.name}_t{args.copy_tile}"
+def copy_profile_name(args, wl, tile=None) -> str:
+    name = f"tile_copy_kernel_{wl.name}_t{args.copy_tile if tile is None else tile}"
     return name + (f"_per{args.copy_per_wg}" if args.copy_per_wg else "") + ".md"
 
 
 def parse_args(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    # The GPU's clocks ramp up over roughly the first 100 launches (30 ms) of
-    # sustained load after idle; the default warmup covers that ramp so the
-    # timed steps see the steady state.
+    # (the clock ramp after idle is covered by each leg's settling phase, so
+    # --warmup is only the extra launches before the timed ones)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=150)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="minimum length of each leg's clock-settling phase")
+    ap.add_argument("--settle-launches", type=int, default=100,
+                    help="minimum launches of each leg's clock-settling phase")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="only the headline legs (no configs array, no per-config oracle)")
+    ap.add_argument("--sweep-steps", type=int, default=20, help="timed launches per configs entry")
     ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
     ap.add_argument("--variant", default="fused_seq",
                     choices=["bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec"])
@@ -109,9 +128,6 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target CPU time of the oracle baseline sample")
-    ap.add_argument("--cpu-configs", action="store_true",
-                    help="also time the oracle on every workload (all host threads, and one "
-                         "thread for the two small ones) and report it as cpu_configs")
     ap.add_argument("--oracle-time", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--oracle-rows", type=int, default=0, help=argparse.SUPPRESS)
     ap.add_argument("--calibrate-traffic", action="store_true",
@@ -119,61 +135,164 @@ def parse_args(argv=None):
     return ap.parse_args(argv)
 
 
+VARIANTS = ("bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec")
+
+# The configs array: (workload, schedule, tile, K slices, producer WGs,
+# consumer WGs).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256)
+# is not repeated here.
+SWEEP = [
+    ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0),
+    ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wave_spec", "256x128", 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "unfused_pc", "256x256", 0, 224, 32),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 248, 8),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 240, 16),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 224, 32),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 208, 48),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 192, 64),
+    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x256", 2, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x128", 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x256", 2, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x128", 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "wave_spec", "256x128", 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "wg_spec", "256x128", 0, 128, 128),
+    ("gas_f16_w8_m8192_k8192_n1024", "unfused_pc", "256x128", 0, 192, 64),
+]
+
+
+class GasCase:
+    """Inputs in HBM, heap and gathered buffers of one workload and tile,
+    reused by every leg with that workload and tile."""
+
+    def __init__(self, torch, sym, workload, wl, tile):
+        self.wl = wl
+        self.tm, self.tn = (int(x) for x in tile.split("x"))
+        A, B = workload.workload_inputs(wl, seed=0)
+        self.A, self.B = A, B
+        self.dA, self.dB = A.cuda(), B.cuda()
+        tiles = -(-wl.M // self.tm) * -(-wl.N_local // self.tn)
+        slot = wl.M * wl.N_gathered * 2 + wl.world * tiles * 4 + (1 << 16)
+        self.heap = sym.Heap(wl.world, slot)
+        self.out = sym.GatheredOutput(self.heap, wl.M, wl.N_local,
+                                      workload.torch_dtype(wl.dtype), self.tm, self.tn)
+
+    def close(self):
+        self.heap.close()
+
+
+def settle(launch, torch, args) -> dict:
+    """Back-to-back launches until at least --settle-launches of them and
+    --settle-ms have run (the clock ramp after idle); returns what ran."""
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        for _ in range(10):
+            launch()
+        n += 10
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
+        if n >= args.settle_launches and ms >= args.settle_ms:
+            return {"launches": n, "ms": round(ms, 1)}
+
+
+def time_back_to_back(launch, torch, steps: int) -> float:
+    """Total ms of `steps` launches back to back between two events on the
+    launch stream (the library launches on torch's current stream).  An event
+    pair around every launch would add a stream barrier (and about 10 us) to
+    each; launches on one stream do not overlap, so the average launch
+    duration is total / steps (it includes the ~2 us between launches)."""
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for _ in range(steps):
+        launch()
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1)
+
+
+def per_call_median_ms(launch, torch, n: int) -> float:
+    """Median of n launches each timed by its own event pair."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    for a, b in evs:
+        a.record()
+        launch()
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in evs)
+
+
+def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps, warmup,
+            label_args) -> dict:
+    """One timed GEMM + All-Scatter configuration on `case`."""
+    wl = case.wl
+    v = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
+         "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[variant]
+    kw = dict(gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, nontemporal=args.nontemporal,
+              group_m=args.group_m, split_k=split_k)
+
+    def launch():
+        case.out.run(case.dA, case.dB, 0, v, **kw)
+
+    st = settle(launch, torch, args)
+    for _ in range(warmup):
+        launch()
+    case.heap.barrier()
+    total_ms = time_back_to_back(launch, torch, steps)
+    case.heap.barrier()        # raises if a device-side wait timed out
+    ms = total_ms / steps
+    tflops = wl.flops / (ms * 1e-3) / 1e12
+    peak = PEAK_MFMA_TFLOPS[wl.dtype]
+    prof = gas_profile_name(label_args, wl)
+    traffic = counter_traffic(prof, KERNEL_SOURCES)
+    return {"ms": ms, "tflops": tflops, "settle": st, "launch": launch,
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": peak, "unit": "TFLOP/s",
+                         "frac": tflops / peak, "traffic": traffic,
+                         "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
+                         "kernel": "gas_kernel<%d,%d,%s>" % (case.tm, case.tn, wl.dtype),
+                         "algorithmic_flops_per_launch": wl.flops,
+                         "algorithmic_bytes_per_launch": gemm_bytes(wl),
+                         "avg_launch_ms": ms}}
+
+
+def gemm_bytes(wl) -> int:
+    """Compulsory bytes of one call: A and B_shard read once, the rank's
+    block written once into each of the w slots."""
+    return 2 * (wl.M * wl.K + wl.K * wl.N_local + wl.world * wl.M * wl.N_local)
+
+
+class _Label:
+    """The argument names gas_profile_name reads, for a configs entry."""
+
+    def __init__(self, args, variant, tile, split_k, gemm_wgs, copy_wgs):
+        self.variant, self.tile, self.split_k = variant, tile, split_k
+        self.gemm_wgs, self.copy_wgs = gemm_wgs, copy_wgs
+        self.nontemporal, self.group_m = args.nontemporal, args.group_m
+
+
 def bench_gas(args, torch, sym, workload):
     wl = workload.GEMM_WORKLOADS[args.workload]
     if args.tile is None:
         args.tile = "256x128" if args.variant == "wave_spec" else "256x256"
-    tm, tn = (int(x) for x in args.tile.split("x"))
-    variant = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
-               "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[args.variant]
-    A, B = workload.workload_inputs(wl, seed=0)
-    dA, dB = A.cuda(), B.cuda()
-    tiles = -(-wl.M // tm) * -(-wl.N_local // tn)
-    slot = wl.M * wl.N_gathered * 2 + wl.world * tiles * 4 + (1 << 16)
-    heap = sym.Heap(wl.world, slot)
-    out = sym.GatheredOutput(heap, wl.M, wl.N_local, workload.torch_dtype(wl.dtype), tm, tn)
-    kw = dict(gemm_wgs=args.gemm_wgs, copy_wgs=args.copy_wgs, nontemporal=args.nontemporal,
-              group_m=args.group_m, split_k=args.split_k)
-
-    def step():
-        out.run(dA, dB, 0, variant, **kw)
-
-    for _ in range(args.warmup):
-        step()
-    heap.barrier()
-    torch.cuda.synchronize()
-
-    # K launches back to back between two events on the launch stream; an
-    # event pair around every launch would add a stream barrier (and about
-    # 10 us) to each.  Launches on one stream do not overlap, so the average
-    # launch duration is total / K (it includes the ~2 us between launches).
-    K = args.steps
-    t_all0 = torch.cuda.Event(enable_timing=True)
-    t_all1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_all0.record()
-    for _ in range(K):
-        step()
-    t_all1.record()
-    torch.cuda.synchronize()
-    heap.barrier()        # raises if a device-side wait timed out
-    total_ms = t_all0.elapsed_time(t_all1)
-    ms_per_step = total_ms / K
-    flops = wl.flops
-    kernel_s = ms_per_step * 1e-3
-    achieved = flops / kernel_s / 1e12
-    peak = PEAK_MFMA_TFLOPS[wl.dtype]
-    prof = gas_profile_name(args, wl)
-    traffic = counter_traffic(prof, KERNEL_SOURCES)
+    case = GasCase(torch, sym, workload, wl, args.tile)
+    r = gas_leg(args, torch, sym, case, args.variant, args.split_k, args.gemm_wgs,
+                args.copy_wgs, args.steps, args.warmup, args)
+    # the per-call median of the measurement convention (one event pair per
+    # call), after the timed region
+    med = per_call_median_ms(r["launch"], torch, 20)
+    case.heap.barrier()
     res = {
-        "value": flops / (ms_per_step * 1e-3) / 1e12,
-        "ms_per_step": ms_per_step,
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": traffic,
-                     "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
-                     "kernel": "gas_kernel<%d,%d,%s>" % (tm, tn, wl.dtype),
-                     "algorithmic_flops_per_launch": flops,
-                     "avg_launch_ms": kernel_s * 1e3},
+        "value": r["tflops"],
+        "ms_per_step": r["ms"],
+        "per_call_median_ms": med,
+        "settle": r["settle"],
+        "roofline": r["roofline"],
         "config": {"workload": wl.name, "M": wl.M, "K": wl.K, "N_local": wl.N_local,
                    "world_size": wl.world, "rank": 0, "N_gathered": wl.N_gathered,
                    "variant": args.variant, "tile": args.tile, "gemm_wgs": args.gemm_wgs,
@@ -181,12 +300,39 @@ def bench_gas(args, torch, sym, workload):
                    "split_k": max(args.split_k, 1)},
         "dtype": wl.dtype,
     }
-    heap.close()
+    A, B = case.A, case.B
+    case.close()
     return res, wl, A, B
 
 
-def bench_copy(args, torch, sym, workload):
+def bench_sweep(args, torch, sym, workload) -> list:
+    """Every SWEEP entry, grouped so each workload and tile's buffers are
+    built once."""
+    out = []
+    cases = {}
+    for name, variant, tile, split_k, g, c in SWEEP:
+        key = (name, tile)
+        if key not in cases:
+            for k in list(cases):
+                cases.pop(k).close()
+            cases[key] = GasCase(torch, sym, workload, workload.GEMM_WORKLOADS[name], tile)
+        case = cases[key]
+        label = _Label(args, variant, tile, split_k, g, c)
+        r = gas_leg(args, torch, sym, case, variant, split_k, g, c, args.sweep_steps, 5, label)
+        wl = case.wl
+        out.append({"workload": name, "dtype": wl.dtype, "schedule": variant, "tile": tile,
+                    "split_k": max(split_k, 1), "gemm_wgs": g, "copy_wgs": c,
+                    "ms": r["ms"], "value": r["tflops"], "unit": "TFLOP/s",
+                    "steps": args.sweep_steps, "settle": r["settle"],
+                    "roofline": r["roofline"]})
+    for k in list(cases):
+        cases.pop(k).close()
+    return out
+
+
+def bench_copy(args, torch, sym, workload, tile=None):
     wl = workload.HEAP_COPY
+    t = args.copy_tile if tile is None else tile
     nbytes = wl.rows * wl.cols * 4
     heap = sym.Heap(wl.world, 2 * nbytes + (1 << 20))
     src, dst = heap.alloc(nbytes), heap.alloc(nbytes)
@@ -195,16 +341,13 @@ def bench_copy(args, torch, sym, workload):
     # Cold runs: read 1 GiB of other data first (more than the 256 MB MALL) so
     # the heap is evicted; a read leaves no dirty lines to write back later.
     flush = torch.ones(1 << 28, dtype=torch.int32, device="cuda")
-    t = args.copy_tile
     stream = sym.current_stream()
 
     def launch():
         sym.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, sym.F32, t, t,
                               wl.shift, -1, flags, tiles_per_wg=args.copy_per_wg, stream=stream)
 
-    for _ in range(200):      # past the clock ramp (see --warmup)
-        launch()
-    torch.cuda.synchronize()
+    st = settle(launch, torch, args)
     # warm launches back to back, then the cold ones, each after the flush;
     # the cold launches are the last copy-iters dispatches of the kernel (the
     # committed rocprofv3 summary averages exactly those)
@@ -232,13 +375,13 @@ def bench_copy(args, torch, sym, workload):
     cold_mean_ms = statistics.fmean(cold)
     warm_ms = sum(warm) / len(warm)
     gbs = moved / (cold_ms * 1e-3) / 1e9
-    prof = copy_profile_name(args, wl)
+    prof = copy_profile_name(args, wl, t)
     traffic = counter_traffic(prof, COPY_SOURCES)
     heap.close()
     del flush
     return {
         "value": gbs, "unit": "GB/s", "tile": f"{t}x{t}", "workload": wl.name,
-        "tiles_per_wg": args.copy_per_wg,
+        "tiles_per_wg": args.copy_per_wg, "settle": st,
         "bytes_per_launch": moved, "cold_ms": cold_ms, "cold_mean_ms": cold_mean_ms,
         "warm_ms": warm_ms,
         "warm_GBps": moved / (warm_ms * 1e-3) / 1e9,
@@ -250,6 +393,18 @@ def bench_copy(args, torch, sym, workload):
 
 
 def cpu_model() -> str:
+    """The host CPU's full model name (lscpu, else /proc/cpuinfo), with the
+    socket count."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        info = dict(l.split(":", 1) for l in out.splitlines() if ":" in l)
+        name = info.get("Model name", "").strip()
+        if name:
+            sockets = info.get("Socket(s)", "").strip()
+            return name + (f" ({sockets} sockets)" if sockets else "")
+    except (OSError, subprocess.SubprocessError, ValueError):
+        pass
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
@@ -279,7 +434,8 @@ def oracle_gemm_rate(wl, rows: int, seconds: float, workload) -> dict:
         done += 1
     flops = 2.0 * rows * wl.N_local * wl.K * done
     return {"value": flops / total / 1e12, "unit": "TFLOP/s", "cores": oracle_threads(),
-            "rows": rows, "of_rows": wl.M, "repetitions": done, "seconds": round(total, 2)}
+            "kind": "oracle", "rows": rows, "of_rows": wl.M, "repetitions": done,
+            "seconds": round(total, 2)}
 
 
 def oracle_time_child(name: str, rows: int, seconds: float, threads: int) -> dict:
@@ -295,9 +451,11 @@ def oracle_time_child(name: str, rows: int, seconds: float, threads: int) -> dic
 
 
 def cpu_configs(args, workload) -> dict:
-    """The oracle on every GEMM workload (bounded row samples of the large
-    ones) with all host threads, and with one thread on the two small ones."""
-    out = {}
+    """The oracle (GEMM + placement + counters) on every GEMM workload with
+    all host threads (the first 512 rows of A where M is larger), and with one
+    thread on the tiny fp16 and the bf16 1024x4096.4096x1024 workloads, each
+    for about a quarter of --cpu-seconds."""
+    out = {"cpu_model": cpu_model()}
     secs = max(1.0, args.cpu_seconds / 4)
     for wl in workload.GEMM_WORKLOADS.values():
         rows = min(wl.M, 512)
@@ -372,9 +530,19 @@ def main(argv=None):
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
     torch.cuda.set_device(0)
-    # The copy leg runs first, each leg after its own warmup: timed right after
-    # the GEMM leg's hundreds of launches, the copy measured ~8% slower.
-    copy = None if args.no_copy else bench_copy(args, torch, sym, workload)
+    # Order: the copy legs (the headline tile last), the configs array, then
+    # the headline GEMM leg, so that the last dispatches of each headline
+    # kernel are its timed ones (the committed rocprofv3 summaries average
+    # those).  Every leg settles the clock first.
+    copies = []
+    if not args.no_copy:
+        if not args.no_sweep:
+            copies = [bench_copy(args, torch, sym, workload, tile=t)
+                      for t in workload.HEAP_COPY.tiles if t != args.copy_tile]
+        copy = bench_copy(args, torch, sym, workload)
+    else:
+        copy = None
+    sweep = [] if args.no_sweep else bench_sweep(args, torch, sym, workload)
     res, wl, A, B = bench_gas(args, torch, sym, workload)
     line = {
         "metric": METRIC,
@@ -391,14 +559,18 @@ def main(argv=None):
         "data": "synthetic",
         "config": res["config"],
         "roofline": res["roofline"],
+        "settle": res["settle"],
+        "per_call_median_ms": res["per_call_median_ms"],
     }
     if copy is not None:
         line["tile_copy"] = copy
         if not args.no_cpu_baseline:
             line["tile_copy"]["cpu_baseline"] = copy_cpu_baseline(args, workload)
+    if copies or sweep:
+        line["configs"] = [dict(c, schedule="heap_copy") for c in copies] + sweep
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args, wl, A, B, workload)
-        if args.cpu_configs:
+        if not args.no_sweep:
             line["cpu_configs"] = cpu_configs(args, workload)
     if args.calibrate_traffic:
         # a plain copy kernel of known size: 256 MiB read + 256 MiB written

@@ -84,7 +84,9 @@ typedef struct {
                              line for the release to write back) */
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
-                             (8 for 128x128 and the 256-row tiles, 4 for 64x64) */
+                             (8 for 128x128 and the 256-row tiles, 4 for 64x64).
+                             Built: 64x64 with 4; 128x128 and 256x128 with 4 or 8;
+                             256x256 and 256x224 with 8 (others EUNSUPPORTED) */
     symtile_stream copy_stream; /* UNFUSED_PC: stream of the copy kernel; NULL = a
                              stream the heap creates on first use.  It must not
                              be the call's stream. */
@@ -108,9 +110,16 @@ typedef struct {
                              aligned, outside the output and counters.  Its first
                              round_up(8 * tiles, 256) bytes are counters that must
                              be zero before the first call that uses it; every
-                             call leaves them zero again (after an ETIMEOUT, zero
-                             them again).  Calls that share a workspace must not
-                             overlap in time (same stream, or synchronised). */
+                             call that completes leaves them zero again.  A call
+                             whose wait timed out (ETIMEOUT) leaves them as they
+                             are, since slices of that call may still count
+                             themselves after the timeout: zero the workspace
+                             after the barrier that reports it.  A later call
+                             that finds them non-zero skips the affected tiles
+                             and reports EINVAL at the next barrier rather than
+                             summing stale partials.  Calls that share a
+                             workspace must not overlap in time (same stream, or
+                             synchronised). */
     size_t workspace_bytes;
 } symtile_gas_config;
 
@@ -186,8 +195,9 @@ symtile_status symtile_translate_device(const symtile_heap* h, const uint64_t* i
 
 /* Host barrier (Section 3.2, barrier): wait for the stream (device when
  * NULL), then read and clear the heap's device error word.  Returns
- * ETIMEOUT if a device-side wait expired since the last barrier, EHIP if
- * the device reported an error. */
+ * ETIMEOUT if a device-side wait expired since the last barrier; EINVAL if a
+ * split-K call found its workspace counters non-zero at entry (that call
+ * skipped the affected tiles); EHIP for any other device error. */
 symtile_status symtile_barrier(symtile_heap* h, symtile_stream s);
 
 /* Fill `bytes` at `offset` of slot `rank` (every slot when rank < 0) with
@@ -234,23 +244,60 @@ symtile_status symtile_value_exercise(symtile_heap* h, int op, size_t src_off, s
                                       size_t bytes, int cur_rank, int remote_rank,
                                       int nontemporal, symtile_stream s);
 
+/* Forms of the message-passing litmus test: how the counters publish and wait. */
+typedef enum {
+    SYMTILE_MP_RELAXED = 0,  /* relaxed +1, relaxed polls, no fences (no guarantee) */
+    SYMTILE_MP_FENCES = 1,   /* release fence + relaxed +1; relaxed polls + acquire fence */
+    SYMTILE_MP_RMW = 2,      /* fetch_add(+1, release); polls by fetch_add(0, acquire) */
+    SYMTILE_MP_CAS = 3       /* cas(i-1 -> i, release); polls by cas(i -> i, acquire), the lock
+                                handshake of the workgroup-specialised listing (Section 4.2.2) */
+} symtile_mp_form;
+
 /* Message-passing litmus test of the flag protocol (Section 3.3.3, memory
- * model).  pairs writer/reader workgroup pairs (pair p: writer rank p % w,
- * reader rank (p + 1) % w, placed on different XCDs) run `rounds` rounds:
- * the writer writes `words` uint32 of a round-specific pattern into the
- * reader's slot at data_off + 4 * words * p, then publishes a counter in the
- * reader's slot (flag_off + 8p) with an agent-scope release; the reader
- * acquires it, checks every word, and acknowledges through a counter in the
- * writer's slot (flag_off + 8p + 4).  ordered = 0 drops the release and
- * acquire fences (relaxed counters only).  result (device, 2 uint32, zeroed
- * by the caller) accumulates [0] words that did not hold the round's value
- * when read and [1] rounds checked.  The counters must be zero on entry.
- * Waits are bounded by spin_limit polls (0 = 1<<22); a timeout records
- * ETIMEOUT for the next symtile_barrier.  EINVAL for bad sizes or regions;
- * EUNSUPPORTED when 2*pairs exceeds the CU count (all must be resident). */
+ * model: atomics with an ordering and a scope).  pairs writer/reader
+ * workgroup pairs (pair p: writer rank p % w, reader rank (p + 1) % w, placed
+ * on different XCDs) run `rounds` rounds: the writer writes `words` uint32 of
+ * a round-specific pattern into the reader's slot at data_off + 4 * words *
+ * p, then publishes a counter in the reader's slot (flag_off + 8p) in the
+ * given form at the given scope (symtile_scope); the reader waits for it,
+ * checks every word, and acknowledges through a counter in the writer's slot
+ * (flag_off + 8p + 4) the same way.  In the RELAXED and FENCES forms the
+ * counters are updated and polled at agent scope or wider (only the data's
+ * ordering depends on `scope`); in RMW and CAS the counters take `scope`.
+ * result (device, 2 uint32, zeroed by the caller) accumulates [0] words that
+ * did not hold the round's value when read and [1] rounds checked.  The
+ * counters must be zero on entry.  Every wait is bounded by spin_limit polls
+ * (0 = 1<<22); a timeout records ETIMEOUT for the next symtile_barrier and
+ * ends the pair (its partner then times out as well).  EINVAL for bad sizes,
+ * regions, form or scope; EUNSUPPORTED when 2*pairs exceeds the CU count
+ * (all must be resident). */
 symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_off, int pairs,
-                                 int rounds, int words, int ordered, uint32_t spin_limit,
+                                 int rounds, int words, int form, int scope, uint32_t spin_limit,
                                  uint32_t* result, symtile_stream s);
+
+/* Forms of the store-buffering litmus test. */
+typedef enum {
+    SYMTILE_SB_RELAXED = 0,  /* relaxed atomic store, relaxed atomic load */
+    SYMTILE_SB_ACQ_REL = 1,  /* exchange and fetch_add(0), both acq_rel */
+    SYMTILE_SB_SEQ_CST = 2   /* seq_cst atomic store, seq_cst atomic load */
+} symtile_sb_form;
+
+/* Store-buffering litmus test (Section 3.3.3, memory model).  pairs pairs of
+ * single threads (pair p: side 0 on rank p % w, side 1 on rank (p + 1) % w,
+ * on different XCDs) run `rounds` rounds; round i of pair p uses the 16
+ * bytes at flag_off + 16 * (p * rounds + i) of the two slots, which must be
+ * zero on entry: x (word 0, side 1's slot), y (word 1, side 0's slot) and an
+ * arrival counter (word 2, side 0's slot).  Both sides arrive and wait for
+ * each other (bounded by spin_limit, 0 = 1<<22), then side 0 writes x = 1 and
+ * reads y while side 1 writes y = 1 and reads x, in the given form at the
+ * given scope.  out (device uint32 [pairs][rounds][2]) receives what each
+ * side read, or 2 for a round not run after a timeout (ETIMEOUT at the next
+ * symtile_barrier).  Both sides reading 0 is forbidden in the ACQ_REL and
+ * SEQ_CST forms.  EINVAL for bad sizes, regions, form or scope;
+ * EUNSUPPORTED when 2*pairs exceeds the CU count. */
+symtile_status symtile_litmus_sb(symtile_heap* h, size_t flag_off, int pairs, int rounds,
+                                 int form, int scope, uint32_t spin_limit, uint32_t* out,
+                                 symtile_stream s);
 
 /* ---- heap tile copy (Section 3.3.2, pointer-based put and get) ------------ */
 

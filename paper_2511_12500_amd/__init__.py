@@ -10,10 +10,11 @@ itself imports without the library, so a fresh checkout can build it.
 """
 _BINDING = (
     "ATOMIC_OPS", "BF16", "BULK_SYNC", "F16", "F32", "FUSED_SEQ", "GET", "LIB_PATH", "LOAD",
-    "PUT", "SCOPES", "SEMS", "STORE",
+    "PUT", "SCOPES", "SEMS", "STORE", "MP_FORMS", "SB_FORMS", "symtile_litmus_sb",
     "TRACE_WORDS", "UNFUSED_PC", "WAVE_SPEC", "WG_SPEC", "GasConfig", "SymtileError", "lib", "symtile_atomic_exercise",
     "symtile_barrier", "symtile_clock_rate_khz", "symtile_device_info",
-    "symtile_gas_workspace_bytes", "symtile_gemm_all_scatter", "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
+    "symtile_gas_workspace_bytes", "symtile_gemm_all_scatter",
+    "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
     "symtile_heap_destroy", "symtile_heap_fill", "symtile_heap_info", "symtile_heap_ptr",
     "symtile_last_error", "symtile_tile_copy", "symtile_translate", "symtile_translate_device",
     "symtile_value_exercise", "symtile_version",

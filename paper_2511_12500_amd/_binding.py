@@ -14,6 +14,8 @@ LOAD, STORE = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}
 SEMS = {"relaxed": 0, "acquire": 1, "release": 2, "acq_rel": 3}
 SCOPES = {"block": 0, "gpu": 1, "sys": 2}
+MP_FORMS = {"relaxed": 0, "fences": 1, "rmw": 2, "cas": 3}
+SB_FORMS = {"relaxed": 0, "acq_rel": 1, "seq_cst": 2}
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ETIMEOUT", -5: "EUNSUPPORTED"}
 
@@ -81,7 +83,8 @@ def _load():
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "symtile_gas_workspace_bytes": [i32, i32, i32, i32, i32, ctypes.POINTER(sz)],
         "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
-        "symtile_litmus_mp": [vp, sz, sz, i32, i32, i32, i32, u32, vp, vp],
+        "symtile_litmus_mp": [vp, sz, sz, i32, i32, i32, i32, i32, u32, vp, vp],
+        "symtile_litmus_sb": [vp, sz, i32, i32, i32, i32, u32, vp, vp],
         "symtile_value_exercise": [vp, i32, sz, sz, sz, i32, i32, i32, vp],
     }
     for name, args in decl.items():
@@ -235,10 +238,18 @@ def symtile_gas_workspace_bytes(M: int, N_local: int, tile_m: int, tile_n: int,
 
 
 def symtile_litmus_mp(h: int, data_off: int, flag_off: int, pairs: int, rounds: int,
-                      words: int, ordered: int, spin_limit: int, result: int,
+                      words: int, form: int, scope: int, spin_limit: int, result: int,
                       stream: int = 0) -> None:
-    _check(lib.symtile_litmus_mp(_vp(h), data_off, flag_off, pairs, rounds, words, ordered,
+    """form: MP_FORMS[...]; scope: SCOPES[...]."""
+    _check(lib.symtile_litmus_mp(_vp(h), data_off, flag_off, pairs, rounds, words, form, scope,
                                  spin_limit, _vp(result), _vp(stream)), "symtile_litmus_mp")
+
+
+def symtile_litmus_sb(h: int, flag_off: int, pairs: int, rounds: int, form: int, scope: int,
+                      spin_limit: int, out: int, stream: int = 0) -> None:
+    """form: SB_FORMS[...]; scope: SCOPES[...]."""
+    _check(lib.symtile_litmus_sb(_vp(h), flag_off, pairs, rounds, form, scope, spin_limit,
+                                 _vp(out), _vp(stream)), "symtile_litmus_sb")
 
 
 def symtile_clock_rate_khz(device: int) -> int:

@@ -265,43 +265,39 @@ __device__ __forceinline__ void with_store_policy(int mode, F&& f) {
         f(std::integral_constant<int, symtile::kStoreDefault>{});
 }
 
+// Geometry of output tile (tm, tn) for the tile verbs: 16-bit elements, so
+// 8 per 16-byte chunk; THREADS threads cover CPR chunk columns per pass.
+template <int BM, int BN, int THREADS>
+__device__ __forceinline__ symtile::TileGeom out_tile(const GasParams& p, int tm, int tn) {
+    using IO = TileIO<BM, BN, THREADS>;
+    symtile::TileGeom g;
+    g.rows = min(BM, p.M - tm * BM);
+    g.chunks = min(BN, p.N - tn * BN) / 8;
+    g.ld_bytes = (uint32_t)p.ldc * 2;
+    g.lg_w = __builtin_ctz(IO::CPR);
+    return g;
+}
+
+// Address of tile (tm, tn) of this rank's column block in the local heap.
+__device__ __forceinline__ uint16_t* out_tile_ptr(const GasParams& p, int BM, int BN, int tm, int tn) {
+    return p.C + (size_t)p.rank * p.N + (size_t)tm * BM * p.ldc + (size_t)tn * BN;
+}
+
 // Copy one finished tile from the local heap to every other heap (the put of
 // Sections 4.1.1 and 4.2.2) and release its counters there.
 template <int BM, int BN, int THREADS, int POLICY>
 __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
     using IO = TileIO<BM, BN, THREADS>;
     const int tid = threadIdx.x;
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
-    const uint16_t* src = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
-    const uint32_t span = tile_span(rows, cols, p.ldc);
-    const symtile::rsrc_t rs = symtile::make_rsrc(src, span);
-    const int c = tid % IO::CPR;
-    const uint32_t voff = (8 * c < cols)
-                              ? (uint32_t)((tid / IO::CPR) * p.ldc * 2 + c * 16)
-                              : symtile::kOOB;
-    const uint32_t pass_bytes = (uint32_t)(IO::RP * p.ldc * 2);
-#pragma unroll 1
-    for (int b = 0; b < IO::PASSES; b += IO::U) {
-        symtile::u32x4 v[IO::U];
-#pragma unroll
-        for (int u = 0; u < IO::U; ++u) v[u] = symtile::buf_ld16(rs, voff, (b + u) * pass_bytes);
-        for (int d = 1; d < p.world; ++d) {
-            const int s = (p.rank + d) % p.world;
-            const symtile::rsrc_t rd =
-                symtile::make_rsrc(symtile::translate(src, p.rank, s, p.bases), span);
-#pragma unroll
-            for (int u = 0; u < IO::U; ++u)
-                symtile::buf_st16p<POLICY>(v[u], rd, voff, (b + u) * pass_bytes);
-        }
-    }
+    symtile::put_ranks<POLICY, IO::U>(out_tile_ptr(p, BM, BN, tm, tn), out_tile<BM, BN, THREADS>(p, tm, tn),
+                                      p.rank, 1, p.world, p.world, p.bases, tid, THREADS);
     symtile::wg_stores_done();
     if (tid < 64) {            // wave 0: one release, then lane d counts slot rank + d
-        symtile::release_agent();
+        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
         uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
         const int d = tid + 1;
         if (d < p.world)
-            symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
+            symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + d) % p.world, p.bases));
     }
 }
 
@@ -321,11 +317,8 @@ __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
         if (tid == 0) {
             if (tr) tr[SYMTILE_TRACE_COPY_WAIT] = symtile::clock_now();
             const bool ok =
-                symtile::flag_wait_geq(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
-            if (ok)
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            else
-                symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+                symtile::flag_wait(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
+            if (!ok) symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
             if (tr) tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
             s_ok = ok;
         }
@@ -398,11 +391,11 @@ __device__ void copy_wave_tiles(const GasParams& p, int KT) {
         };
         auto publish = [&]() {
             __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            symtile::release_agent();           // one release; lane d counts slot rank + d
+            symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();  // one release; lane d counts slot rank + d
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + ptm) * p.tiles_n + ptn;
             if (lane >= 1 && lane < p.world)
-                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + lane) % p.world,
-                                                     p.bases));
+                symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + lane) % p.world,
+                                                        p.bases));
             if (lane == 0 && p.trace)
                 tile_trace(p, ptm, ptn)[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
         };
@@ -568,9 +561,12 @@ void gas_kernel(const GasParams p) {
         const int kbeg = kt0 * BK, kend = p.K - kbeg;
         const symtile::i32x4_t rA = symtile::make_rsrc_words(
             p.A + (size_t)m0 * p.lda + kbeg, (uint32_t)(rows_a * p.lda * 2 - kbeg * 2));
+        // B's resource ends at the shard's last element (row K-1, column
+        // N-1), so with ldb > N the staged columns past N of the last row
+        // read zero instead of touching memory past a tightly sized B.
         const symtile::i32x4_t rB = symtile::make_rsrc_words(
             p.B + (size_t)kbeg * p.ldb + n0,
-            kend > 0 ? (uint32_t)((size_t)kend * p.ldb * 2 - (size_t)n0 * 2) : 0u);
+            kend > 0 ? (uint32_t)(((size_t)(kend - 1) * p.ldb + p.N - n0) * 2) : 0u);
 
         acc_t acc[MI][NI];
 #pragma unroll
@@ -773,7 +769,15 @@ void gas_kernel(const GasParams p) {
             if (tid == 0)
                 s_ticket = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
             __syncthreads();
-            const bool last = __builtin_amdgcn_readfirstlane(s_ticket) + 1 == (uint32_t)p.split;
+            const uint32_t ticket = __builtin_amdgcn_readfirstlane(s_ticket);
+            if (ticket >= (uint32_t)p.split) {
+                // more arrivals than slices: the counters were not zero at
+                // the start of this call (a timed-out call leaves them so);
+                // nothing of this tile can be trusted, so report and skip it
+                if (tid == 0) symtile::raise_error(p.err, symtile::ERR_WORKSPACE);
+                continue;
+            }
+            const bool last = ticket + 1 == (uint32_t)p.split;
             // Partial tile of slice q: each thread's accumulators, 16 bytes
             // per (i, j, 4-value group), so a wave's access is 1 KiB contiguous.
             auto slot = [&](int q) {
@@ -829,22 +833,24 @@ void gas_kernel(const GasParams p) {
             if (!last) {
                 put_partial(ks);
                 symtile::wg_stores_done();
-                if (tid == 0) {
-                    symtile::release_agent();
-                    symtile::flag_add(cnt + 1);
-                }
+                if (tid == 0) symtile::flag_publish(cnt + 1);
                 continue;
             }
             if (tid == 0) {
-                const bool ok = symtile::flag_wait_geq(cnt + 1, (uint32_t)p.split - 1, p.spin_limit);
-                if (ok)
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-                else
+                const bool ok = symtile::flag_wait(cnt + 1, (uint32_t)p.split - 1, p.spin_limit);
+                if (ok) {
+                    // every slice of this call has counted itself: the next
+                    // call starts again from zero
+                    symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
+                    symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                } else {
+                    // a slice that holds a ticket may still count itself
+                    // later, so the counters are left as they are: the next
+                    // call that uses this workspace then draws tickets past
+                    // the slice count and reports ERR_WORKSPACE instead of
+                    // summing stale partials, until the caller zeroes them
                     symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
-                // every slice of this call has counted itself: the next call
-                // starts again from zero
-                symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
-                symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                }
                 s_ok = ok;
             }
             __syncthreads();
@@ -908,13 +914,12 @@ void gas_kernel(const GasParams p) {
         // rest during the next tile), except for this workgroup's last tile.
         const int n_dst =
             (p.role == ROLE_FUSED || (CW && t + G >= p.num_tiles)) ? p.world : 1;
-        const int rows = min(BM, p.M - m0), cols = min(BN, p.N - n0);
-        const uint16_t* tile_local = p.C + (size_t)p.rank * p.N + (size_t)m0 * p.ldc + n0;
-        const uint32_t span = tile_span(rows, cols, p.ldc);
+        const uint16_t* tile_local = out_tile_ptr(p, BM, BN, tm, tn);
+        const symtile::TileGeom geom = out_tile<BM, BN, THREADS>(p, tm, tn);
+        const symtile::TileLanes lanes = symtile::tile_lanes(geom, tid, THREADS);
         const int c = tid % IO::CPR, r0 = tid / IO::CPR;
-        const uint32_t voff =
-            (8 * c < cols) ? (uint32_t)(r0 * p.ldc * 2 + c * 16) : symtile::kOOB;
-        const uint32_t pass_bytes = (uint32_t)(IO::RP * p.ldc * 2);
+        const uint32_t voff = lanes.voff;
+        const uint32_t pass_bytes = lanes.pass_bytes;
         const uint8_t* crow = Cs + r0 * CROW + ((c ^ (r0 & 7)) << 4);
 #pragma unroll 1
         for (int b = 0; b < IO::PASSES; b += IO::U) {
@@ -923,9 +928,8 @@ void gas_kernel(const GasParams p) {
             for (int u = 0; u < IO::U; ++u)
                 v[u] = *reinterpret_cast<const symtile::u32x4*>(crow + (b + u) * IO::RP * CROW);
             for (int d = 0; d < n_dst; ++d) {
-                const int s = (p.rank + d) % p.world;
                 const symtile::rsrc_t rd =
-                    symtile::make_rsrc(symtile::translate(tile_local, p.rank, s, p.bases), span);
+                    symtile::tile_rsrc(tile_local, geom, p.rank, (p.rank + d) % p.world, p.bases);
                 with_store_policy(p.nontemporal, [&](auto pol) {
 #pragma unroll
                     for (int u = 0; u < IO::U; ++u)
@@ -937,11 +941,11 @@ void gas_kernel(const GasParams p) {
         symtile::wg_stores_done();     // also orders the LDS reads above before reuse
         if (tid < 64) {                // wave 0: one release, then lane d counts slot rank + d
             if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
-            symtile::release_agent();
+            symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
             if (tid < n_dst)
-                symtile::flag_add(symtile::translate(flag, p.rank, (p.rank + tid) % p.world, p.bases));
-            if (tid == 0 && p.role == ROLE_WG_SPEC) symtile::flag_add(p.ready + tm * p.tiles_n + tn);
+                symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + tid) % p.world, p.bases));
+            if (tid == 0 && p.role == ROLE_WG_SPEC) symtile::flag_signal(p.ready + tm * p.tiles_n + tn);
             if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
         }
     }
@@ -1004,6 +1008,8 @@ Variant make_variant() {
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
+// 256x256 tiles are built with 8 waves only: with 4 waves each wave holds a
+// 128x128 block (256 accumulator registers) and the compiler spills it.
 const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
     static const Variant table[] = {
         make_variant<64, 64, false, 4>(),    make_variant<64, 64, true, 4>(),
@@ -1012,7 +1018,6 @@ const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
         make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),
         make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
-        make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
         make_variant<256, 224, false, 8, 16>(), make_variant<256, 224, true, 8, 16>(),
     };
     for (const Variant& v : table)

@@ -250,23 +250,79 @@ int cu_count(int device) {
 // Message-passing litmus test of the flag protocol (Section 3.3.3, memory
 // model): pair p = workgroups 2p (writer, rank p % w) and 2p+1 (reader, rank
 // (p + 1) % w); consecutive workgroup ids land on different XCDs, whose L2s
-// are not coherent with each other.  Round i: the writer waits for ack >= i-1
-// (acquire), writes the round's pattern into the reader's slot, waits for its
-// stores and release-publishes ready = i; the reader waits for ready >= i
-// (acquire), checks every word, counts mismatches, and release-publishes
-// ack = i in the writer's slot.  The data words are plain stores and loads,
-// as the tile data of the GEMM and copy kernels are.  ordered = 0 drops the
-// fences (relaxed flags only), the unsynchronised form the protocol exists to
-// prevent; compiler barriers keep program order there, so what the test sees
-// is the hardware's.
+// are not coherent with each other.  Round i: the writer waits until
+// ack == i-1, writes the round's pattern into the reader's slot, waits for its
+// stores and publishes ready = i; the reader waits until ready == i, checks
+// every word, counts mismatches, and publishes ack = i in the writer's slot.
+// The data words are plain stores and loads, as the tile data of the GEMM
+// and copy kernels are.  How the counters publish and wait is the form:
+//   RELAXED  relaxed +1, relaxed polls, no fences: the unsynchronised form
+//            the protocol exists to prevent;
+//   FENCES   release fence at SCOPE then relaxed +1; relaxed polls then an
+//            acquire fence at SCOPE (the kernels' protocol);
+//   RMW      the ordering carried by the read-modify-writes themselves:
+//            fetch_add(+1, release, SCOPE) publishes, fetch_add(0, acquire,
+//            SCOPE) polls;
+//   CAS      the lock handshake of the workgroup-specialised listing:
+//            cas(i-1 -> i, release, SCOPE) publishes, cas(i -> i, acquire,
+//            SCOPE) polls until it observes i.
+// In RELAXED and FENCES the counters themselves are updated and polled at
+// agent scope or wider, so that only the data's ordering depends on SCOPE;
+// in RMW and CAS the counters take SCOPE too.  Compiler barriers keep
+// program order in every form, so what the test sees is the hardware's.  A
+// wait that exceeds spin_limit polls records ETIMEOUT and ends that
+// workgroup; its partner then times out too, so the kernel always ends.
 __device__ __forceinline__ uint32_t litmus_word(uint32_t round, uint32_t j) {
     return (round * 0x9E3779B1u) ^ (j * 0x85EBCA77u) ^ 0x5bd1e995u;
 }
 
+template <int SCOPE>
+constexpr int at_least_agent() {
+    return SCOPE == __HIP_MEMORY_SCOPE_SYSTEM ? __HIP_MEMORY_SCOPE_SYSTEM : __HIP_MEMORY_SCOPE_AGENT;
+}
+
+// Wait (one thread) until the counter reaches `target` (== target for CAS).
+template <int SCOPE>
+__device__ bool mp_wait(int form, uint32_t* flag, uint32_t target, uint32_t spin_limit) {
+    constexpr int WIDE = at_least_agent<SCOPE>();
+    if (form == SYMTILE_MP_RELAXED) return symtile::flag_poll<WIDE>(flag, target, spin_limit);
+    if (form == SYMTILE_MP_FENCES) {
+        if (!symtile::flag_poll<WIDE>(flag, target, spin_limit)) return false;
+        symtile::fence_acquire<SCOPE>();
+        return true;
+    }
+    for (uint32_t n = 0; n < spin_limit; ++n) {
+        if (form == SYMTILE_MP_RMW) {
+            if (symtile::atomic_add<__ATOMIC_ACQUIRE, SCOPE>(flag, 0u) >= target) return true;
+        } else if (symtile::atomic_cas<__ATOMIC_ACQUIRE, SCOPE>(flag, target, target) == target) {
+            return true;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+// Publish round i (one thread, after the workgroup's accesses are done).
+template <int SCOPE>
+__device__ void mp_publish(int form, uint32_t* flag, uint32_t i) {
+    constexpr int WIDE = at_least_agent<SCOPE>();
+    if (form == SYMTILE_MP_RELAXED) {
+        symtile::flag_signal<WIDE>(flag);
+    } else if (form == SYMTILE_MP_FENCES) {
+        symtile::fence_release<SCOPE>();
+        symtile::flag_signal<WIDE>(flag);
+    } else if (form == SYMTILE_MP_RMW) {
+        symtile::atomic_add<__ATOMIC_RELEASE, SCOPE>(flag, 1u);
+    } else {
+        symtile::atomic_cas<__ATOMIC_RELEASE, SCOPE>(flag, i - 1, i);
+    }
+}
+
+template <int SCOPE>
 __global__ __launch_bounds__(256) void litmus_mp_kernel(const uint64_t* bases, uint32_t* err,
                                                         int world, uint64_t data_off,
                                                         uint64_t flag_off, int rounds, int words,
-                                                        int ordered, uint32_t spin_limit,
+                                                        int form, uint32_t spin_limit,
                                                         uint32_t* result) {
     __shared__ int s_ok;
     __shared__ uint32_t s_bad;
@@ -283,43 +339,90 @@ __global__ __launch_bounds__(256) void litmus_mp_kernel(const uint64_t* bases, u
     uint32_t* ack = symtile::translate(ack_me, me, wr, bases);      // in the writer's slot
     const int tid = threadIdx.x;
     if (tid == 0) s_bad = 0;
+    int done = 0;
     for (int i = 1; i <= rounds; ++i) {
         if (tid == 0) {
-            const bool ok = writer ? symtile::flag_wait_geq(ack, (uint32_t)(i - 1), spin_limit)
-                                   : symtile::flag_wait_geq(ready, (uint32_t)i, spin_limit);
-            if (ok && ordered) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            const bool ok = writer ? mp_wait<SCOPE>(form, ack, (uint32_t)(i - 1), spin_limit)
+                                   : mp_wait<SCOPE>(form, ready, (uint32_t)i, spin_limit);
             if (!ok) symtile::raise_error(err, symtile::ERR_TIMEOUT);
             s_ok = ok;
         }
         __syncthreads();
-        if (!s_ok) return;
+        if (!s_ok) break;
         asm volatile("" ::: "memory");
         if (writer) {
             for (int j = tid; j < words; j += blockDim.x)
                 *symtile::global_ptr(data + j) = litmus_word(i, j);
             symtile::wg_stores_done();
-            if (tid == 0) {
-                if (ordered) symtile::release_agent();
-                symtile::flag_add(ready);
-            }
+            if (tid == 0) mp_publish<SCOPE>(form, ready, (uint32_t)i);
         } else {
             uint32_t bad = 0;
             for (int j = tid; j < words; j += blockDim.x)
                 bad += *symtile::global_ptr(data + j) != litmus_word(i, j);
             if (bad) atomicAdd(&s_bad, bad);
             __syncthreads();                 // every word read before the ack
-            if (tid == 0) {
-                if (ordered) symtile::release_agent();
-                symtile::flag_add(ack);
-            }
+            if (tid == 0) mp_publish<SCOPE>(form, ack, (uint32_t)i);
         }
+        done = i;
     }
     __syncthreads();
     if (tid == 0 && !writer) {
         __hip_atomic_fetch_add(symtile::global_ptr(result), s_bad, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(symtile::global_ptr(result + 1), (uint32_t)rounds,
+        __hip_atomic_fetch_add(symtile::global_ptr(result + 1), (uint32_t)done,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Store-buffering litmus test (Section 3.3.3, memory model): pair p =
+// workgroups 2p (side 0, rank p % w) and 2p+1 (side 1, rank (p + 1) % w), one
+// thread each, on different XCDs.  Round i uses fresh zeroed words x, y (x in
+// side 1's slot, y in side 0's) and an arrival counter: both sides arrive and
+// wait for each other (bounded, agent scope), then side 0 writes x = 1 and
+// reads y, side 1 writes y = 1 and reads x, and each records what it read.
+// Forms: RELAXED = relaxed atomic store and load at SCOPE; ACQ_REL = an
+// exchange and a fetch_add(0), both acq_rel at SCOPE (read-modify-writes
+// read the latest value, and a release RMW read by an acquire RMW
+// synchronises, so both reading 0 is forbidden); SEQ_CST = seq_cst store and
+// load at SCOPE (both reading 0 is forbidden).  out[(p * rounds + i) * 2 +
+// side] receives the value read, or 2 when the round was not run (timeout).
+template <int SCOPE>
+__global__ __launch_bounds__(64) void litmus_sb_kernel(const uint64_t* bases, uint32_t* err,
+                                                       int world, uint64_t flag_off, int rounds,
+                                                       int form, uint32_t spin_limit,
+                                                       uint32_t* out) {
+    if (threadIdx.x != 0) return;
+    const int pair = blockIdx.x >> 1, side = blockIdx.x & 1;
+    const int r0 = pair % world, r1 = (pair + 1) % world;
+    const int me = side ? r1 : r0;
+    bool ok = true;
+    for (int i = 0; i < rounds; ++i) {
+        uint32_t* base_me =
+            reinterpret_cast<uint32_t*>(bases[me] + flag_off) + ((size_t)pair * rounds + i) * 4;
+        uint32_t* x = symtile::translate(base_me, me, r1, bases);         // side 1's slot
+        uint32_t* y = symtile::translate(base_me, me, r0, bases) + 1;     // side 0's slot
+        uint32_t* arrive = symtile::translate(base_me, me, r0, bases) + 2;
+        uint32_t* mine = side ? y : x;
+        uint32_t* other = side ? x : y;
+        uint32_t seen = 2;
+        if (ok) {
+            symtile::flag_signal(arrive);
+            ok = symtile::flag_poll(arrive, 2u, spin_limit);
+            if (!ok) symtile::raise_error(err, symtile::ERR_TIMEOUT);
+        }
+        if (ok) {
+            if (form == SYMTILE_SB_RELAXED) {
+                __hip_atomic_store(symtile::global_ptr(mine), 1u, __ATOMIC_RELAXED, SCOPE);
+                seen = __hip_atomic_load(symtile::global_ptr(other), __ATOMIC_RELAXED, SCOPE);
+            } else if (form == SYMTILE_SB_ACQ_REL) {
+                symtile::atomic_xchg<__ATOMIC_ACQ_REL, SCOPE>(mine, 1u);
+                seen = symtile::atomic_add<__ATOMIC_ACQ_REL, SCOPE>(other, 0u);
+            } else {
+                __hip_atomic_store(symtile::global_ptr(mine), 1u, __ATOMIC_SEQ_CST, SCOPE);
+                seen = __hip_atomic_load(symtile::global_ptr(other), __ATOMIC_SEQ_CST, SCOPE);
+            }
+        }
+        out[((size_t)pair * rounds + i) * 2 + side] = seen;
     }
 }
 
@@ -449,8 +552,15 @@ symtile_status symtile_barrier(symtile_heap* h, symtile_stream s) {
         const uint32_t zero = 0;
         SYMTILE_HIP(hipMemcpy(h->dev_err, &zero, sizeof zero, hipMemcpyHostToDevice));
         if (err & symtile::ERR_TIMEOUT)
-            return symtile_host::fail(SYMTILE_ETIMEOUT,
-                                      "a device-side wait exceeded its spin limit");
+            return symtile_host::fail(
+                SYMTILE_ETIMEOUT,
+                std::string("a device-side wait exceeded its spin limit") +
+                    ((err & symtile::ERR_WORKSPACE) ? "; a split-K workspace was not zeroed" : ""));
+        if (err & symtile::ERR_WORKSPACE)
+            return symtile_host::fail(
+                SYMTILE_EINVAL,
+                "split-K workspace counters were not zero when a call started (zero the "
+                "workspace after an ETIMEOUT); the affected tiles were not written");
         return symtile_host::fail(SYMTILE_EHIP, "device error word " + std::to_string(err));
     }
     return SYMTILE_OK;
@@ -485,11 +595,15 @@ symtile_status symtile_heap_fill(symtile_heap* h, int rank, size_t offset, size_
 }
 
 symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_off, int pairs,
-                                 int rounds, int words, int ordered, uint32_t spin_limit,
+                                 int rounds, int words, int form, int scope, uint32_t spin_limit,
                                  uint32_t* result, symtile_stream s) {
     if (symtile_status st = check_heap(h)) return st;
     if (pairs < 1 || pairs > 256 || rounds < 1 || words < 1 || words > (1 << 20))
         return symtile_host::fail(SYMTILE_EINVAL, "pairs in [1, 256], rounds >= 1, words in [1, 2^20]");
+    if (form < SYMTILE_MP_RELAXED || form > SYMTILE_MP_CAS)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown message-passing form");
+    if (scope < SYMTILE_SCOPE_BLOCK || scope > SYMTILE_SCOPE_SYS)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown scope");
     if (!result) return symtile_host::fail(SYMTILE_EINVAL, "result is NULL");
     const size_t data_bytes = (size_t)pairs * words * 4, flag_bytes = (size_t)pairs * 8;
     if (data_off % 4 || flag_off % 4 || data_off > h->slot_stride ||
@@ -500,10 +614,44 @@ symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_o
     if (2 * pairs > symtile_host::cu_count(h->device))
         return symtile_host::fail(SYMTILE_EUNSUPPORTED, "more workgroups than CUs (all must be resident)");
     DeviceGuard guard(h->device);
-    hipLaunchKernelGGL(litmus_mp_kernel, dim3(2 * pairs), dim3(256), 0,
-                       static_cast<hipStream_t>(s), h->dev_bases, h->dev_err, h->world,
-                       (uint64_t)data_off, (uint64_t)flag_off, rounds, words, ordered ? 1 : 0,
-                       spin_limit ? spin_limit : (1u << 22), result);
+    auto launch = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(2 * pairs), dim3(256), 0, static_cast<hipStream_t>(s),
+                           h->dev_bases, h->dev_err, h->world, (uint64_t)data_off,
+                           (uint64_t)flag_off, rounds, words, form,
+                           spin_limit ? spin_limit : (1u << 22), result);
+    };
+    if (scope == SYMTILE_SCOPE_BLOCK) launch(litmus_mp_kernel<__HIP_MEMORY_SCOPE_WORKGROUP>);
+    else if (scope == SYMTILE_SCOPE_GPU) launch(litmus_mp_kernel<__HIP_MEMORY_SCOPE_AGENT>);
+    else launch(litmus_mp_kernel<__HIP_MEMORY_SCOPE_SYSTEM>);
+    SYMTILE_HIP(hipGetLastError());
+    return SYMTILE_OK;
+}
+
+symtile_status symtile_litmus_sb(symtile_heap* h, size_t flag_off, int pairs, int rounds,
+                                 int form, int scope, uint32_t spin_limit, uint32_t* out,
+                                 symtile_stream s) {
+    if (symtile_status st = check_heap(h)) return st;
+    if (pairs < 1 || pairs > 256 || rounds < 1 || rounds > (1 << 16))
+        return symtile_host::fail(SYMTILE_EINVAL, "pairs in [1, 256], rounds in [1, 65536]");
+    if (form < SYMTILE_SB_RELAXED || form > SYMTILE_SB_SEQ_CST)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown store-buffering form");
+    if (scope < SYMTILE_SCOPE_BLOCK || scope > SYMTILE_SCOPE_SYS)
+        return symtile_host::fail(SYMTILE_EINVAL, "unknown scope");
+    if (!out) return symtile_host::fail(SYMTILE_EINVAL, "out is NULL");
+    const size_t bytes = (size_t)pairs * rounds * 16;
+    if (flag_off % 16 || flag_off > h->slot_stride || bytes > h->slot_stride - flag_off)
+        return symtile_host::fail(SYMTILE_EINVAL, "words misaligned or outside the slot");
+    if (2 * pairs > symtile_host::cu_count(h->device))
+        return symtile_host::fail(SYMTILE_EUNSUPPORTED, "more workgroups than CUs (all must be resident)");
+    DeviceGuard guard(h->device);
+    auto launch = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3(2 * pairs), dim3(64), 0, static_cast<hipStream_t>(s),
+                           h->dev_bases, h->dev_err, h->world, (uint64_t)flag_off, rounds, form,
+                           spin_limit ? spin_limit : (1u << 22), out);
+    };
+    if (scope == SYMTILE_SCOPE_BLOCK) launch(litmus_sb_kernel<__HIP_MEMORY_SCOPE_WORKGROUP>);
+    else if (scope == SYMTILE_SCOPE_GPU) launch(litmus_sb_kernel<__HIP_MEMORY_SCOPE_AGENT>);
+    else launch(litmus_sb_kernel<__HIP_MEMORY_SCOPE_SYSTEM>);
     SYMTILE_HIP(hipGetLastError());
     return SYMTILE_OK;
 }

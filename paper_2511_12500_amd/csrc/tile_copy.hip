@@ -59,52 +59,6 @@ struct CopyParams {
     int band_lg_w;           // >= 0: each run is one rectangle, 1 << band_lg_w chunks wide
 };
 
-// Move `passes` passes of one 16-byte chunk per thread (pass b at byte
-// offset voff + b * pass_bytes in both resources), kBatch passes per batch.
-// Passes past the last one lie beyond the resources (zero loads, dropped
-// stores).  Software-pipelined: the loads of batch i+1 are issued before the
-// stores of batch i.  Loads and stores share one in-order completion
-// counter, so in the plain order (load i, store i, load i+1) the wait for
-// batch i+1's data would also wait for batch i's store acknowledgements; in
-// this order the wait before storing batch i leaves the newer loads and
-// stores in flight.  The loop body has no branch, so the compiler's waits
-// stay exact.
-template <int POLICY>
-__device__ __forceinline__ void copy_passes(symtile::rsrc_t rs, symtile::rsrc_t rd, uint32_t voff,
-                                            uint32_t pass_bytes, int passes) {
-    const int nb = (passes + kBatch - 1) / kBatch;
-    if (nb <= 0) return;
-    u32x4 x[kBatch], y[kBatch];      // batches alternate between x and y (no register moves)
-    auto load = [&](u32x4 (&v)[kBatch], int batch) {
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-            v[u] = symtile::buf_ld16(rs, voff, (uint32_t)(batch * kBatch + u) * pass_bytes);
-    };
-    auto store = [&](const u32x4 (&v)[kBatch], int batch) {
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u)
-            symtile::buf_st16p<POLICY>(v[u], rd, voff, (uint32_t)(batch * kBatch + u) * pass_bytes);
-    };
-    load(x, 0);
-    int i = 0;
-    for (; i + 2 < nb; i += 2) {     // batch i in x; batches i+1, i+2 exist
-        load(y, i + 1);
-        store(x, i);
-        load(x, i + 2);
-        store(y, i + 1);
-    }
-    if (i + 1 < nb) {
-        load(y, i + 1);
-        store(x, i);
-        store(y, i + 1);
-    } else {
-        store(x, i);
-    }
-}
-
-// Copy tile `tile` of source rank r to rank dst.  TC = 16-byte chunks per
-// tile row when it divides the thread count (thread t keeps chunk column
-// t % TC), or 0 for any other width.
 // Source and destination ranks of executing rank r.
 __device__ __forceinline__ void copy_ranks(const CopyParams& p, int r, int& src, int& dst) {
     const int peer_up = ((r + p.shift) % p.world + p.world) % p.world;
@@ -113,77 +67,61 @@ __device__ __forceinline__ void copy_ranks(const CopyParams& p, int r, int& src,
     dst = (p.mode == SYMTILE_GET) ? r : peer_up;
 }
 
+// Copy the nrows x nchunks block at (row0, chunk0) of the matrix from rank
+// src_rank to rank dst with the tile verb `copy`: both buffers are symmetric
+// objects named by their address in rank r's heap, and the verb translates
+// them.  With lg_w >= 0 a pass covers 1 << lg_w chunk columns of
+// kThreads >> lg_w rows, so a run of horizontally adjacent tiles streams
+// whole row segments (up to 8 KiB); lg_w < 0 (a tile width that is not a
+// power of two of chunks) numbers the chunks row-major through the block.
+template <int POLICY>
+__device__ __forceinline__ void copy_block(const CopyParams& p, int r, int src_rank, int dst,
+                                           int row0, int chunk0, int nrows, int nchunks,
+                                           int lg_w) {
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
+                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    uint8_t* dst_local = reinterpret_cast<uint8_t*>(p.bases[r] + p.dst_off) +
+                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
+    symtile::TileGeom g;
+    g.rows = nrows;
+    g.chunks = nchunks;
+    g.ld_bytes = (uint32_t)p.ld_bytes;
+    g.lg_w = lg_w;
+    if (lg_w >= 0) {
+        symtile::copy<POLICY, kBatch>(src, dst_local, g, src_rank, dst, r, p.bases, threadIdx.x,
+                                      kThreads);
+        return;
+    }
+    const symtile::rsrc_t rs = symtile::tile_rsrc(src, g, r, src_rank, p.bases);
+    const symtile::rsrc_t rd = symtile::tile_rsrc(dst_local, g, r, dst, p.bases);
+    const int total = nrows * p.tile_chunks;
+    for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
+        u32x4 v[kBatch];
+        uint32_t off[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = base + u * kThreads;
+            const int row = q / p.tile_chunks, c = q - row * p.tile_chunks;
+            off[u] = (q < total && c < nchunks) ? (uint32_t)(row * p.ld_bytes + c * 16)
+                                                : symtile::kOOB;
+            v[u] = symtile::buf_ld16(rs, off[u], 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) symtile::buf_st16p<POLICY>(v[u], rd, off[u], 0);
+    }
+}
+
+// Copy tile `tile` of rank r (TC = 16-byte chunks per tile row when that is a
+// power of two dividing the thread count, else 0).
 template <int TC, int POLICY>
 __device__ __forceinline__ void copy_one_tile(const CopyParams& p, int r, int src_rank, int dst,
                                               int tile) {
     const int tr = tile / p.tiles_c, tc = tile - tr * p.tiles_c;
     const int row0 = tr * p.tile_r;
     const int chunk0 = tc * p.tile_chunks;
-    const int nrows = min(p.tile_r, p.rows - row0);
-    const int nchunks = min(p.tile_chunks, p.row_chunks - chunk0);
-
-    // Both buffers are symmetric objects named by their address in rank r's
-    // heap, translated into the heaps of src_rank and dst.
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
-                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
-    const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
-                               (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
-    const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
-    const symtile::rsrc_t rs =
-        symtile::make_rsrc(symtile::translate(src, r, src_rank, p.bases), span);
-    const symtile::rsrc_t rd =
-        symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
-
-    if constexpr (TC > 0) {
-        constexpr int RP = kThreads / TC;                  // tile rows per pass
-        const int c = threadIdx.x % TC;
-        const uint32_t voff = (c < nchunks) ? (uint32_t)((threadIdx.x / TC) * p.ld_bytes + c * 16)
-                                            : symtile::kOOB;
-        const uint32_t pass_bytes = (uint32_t)(RP * p.ld_bytes);
-        const int passes = (nrows + RP - 1) / RP;
-        copy_passes<POLICY>(rs, rd, voff, pass_bytes, passes);
-    } else {
-        const int total = nrows * p.tile_chunks;
-        for (int base = threadIdx.x; base < total; base += kThreads * kBatch) {
-            u32x4 v[kBatch];
-            uint32_t off[kBatch];
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
-                const int q = base + u * kThreads;
-                const int row = q / p.tile_chunks, c = q - row * p.tile_chunks;
-                off[u] = (q < total && c < nchunks) ? (uint32_t)(row * p.ld_bytes + c * 16)
-                                                    : symtile::kOOB;
-                v[u] = symtile::buf_ld16(rs, off[u], 0);
-            }
-#pragma unroll
-            for (int u = 0; u < kBatch; ++u) symtile::buf_st16p<POLICY>(v[u], rd, off[u], 0);
-        }
-    }
-}
-
-// Copy the rows x nchunks rectangle at (row0, chunk0) of rank r to rank dst
-// in row-major order: consecutive threads take consecutive 16-byte chunks of
-// a row (a row of up to W = 1 << lg_w chunks per pass group), so a run of
-// horizontally adjacent tiles streams whole row segments of up to 8 KiB.
-template <int POLICY>
-__device__ __forceinline__ void copy_rect(const CopyParams& p, int r, int src_rank, int dst, int row0,
-                                          int chunk0, int nrows, int nchunks, int lg_w) {
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(p.bases[r] + p.src_off) +
-                         (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
-    const uint8_t* dst_local = reinterpret_cast<const uint8_t*>(p.bases[r] + p.dst_off) +
-                               (size_t)row0 * p.ld_bytes + (size_t)chunk0 * 16;
-    const uint32_t span = (uint32_t)((size_t)(nrows - 1) * p.ld_bytes + (size_t)nchunks * 16);
-    const symtile::rsrc_t rs =
-        symtile::make_rsrc(symtile::translate(src, r, src_rank, p.bases), span);
-    const symtile::rsrc_t rd =
-        symtile::make_rsrc(symtile::translate(dst_local, r, dst, p.bases), span);
-    const int c = threadIdx.x & ((1 << lg_w) - 1);
-    const int rp = kThreads >> lg_w;                       // rows per pass
-    const uint32_t voff = (c < nchunks) ? (uint32_t)((threadIdx.x >> lg_w) * p.ld_bytes + c * 16)
-                                        : symtile::kOOB;
-    const uint32_t pass_bytes = (uint32_t)(rp * p.ld_bytes);
-    const int passes = (nrows + rp - 1) / rp;
-    copy_passes<POLICY>(rs, rd, voff, pass_bytes, passes);
+    copy_block<POLICY>(p, r, src_rank, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
+                       min(p.tile_chunks, p.row_chunks - chunk0),
+                       TC > 0 ? __builtin_ctz(TC) : -1);
 }
 
 template <int TC, int POLICY>
@@ -198,8 +136,8 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
         const int t0 = first % p.ntiles;
         const int tr = t0 / p.tiles_c, tc = t0 - tr * p.tiles_c;
         const int row0 = tr * p.tile_r, chunk0 = tc * p.tile_chunks;
-        copy_rect<POLICY>(p, r, src, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
-                      min(p.per_wg * p.tile_chunks, p.row_chunks - chunk0), p.band_lg_w);
+        copy_block<POLICY>(p, r, src, dst, row0, chunk0, min(p.tile_r, p.rows - row0),
+                           min(p.per_wg * p.tile_chunks, p.row_chunks - chunk0), p.band_lg_w);
     } else {
         for (int it = first; it < last; ++it) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
@@ -214,14 +152,14 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
     // thread issuing them one after another into the same cache lines.
     symtile::wg_stores_done();
     if (threadIdx.x < 64) {
-        symtile::release_agent();
+        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
         for (int it = first + (int)threadIdx.x; it < last; it += 64) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
             int src, dst;
             copy_ranks(p, r, src, dst);
             uint32_t* flag_local =
                 reinterpret_cast<uint32_t*>(p.bases[r] + p.flag_off) + it % p.ntiles;
-            symtile::flag_add(symtile::translate(flag_local, r, dst, p.bases));
+            symtile::flag_signal(symtile::translate(flag_local, r, dst, p.bases));
         }
     }
 }

@@ -30,6 +30,7 @@ class Heap:
                                                self.mem.numel())
         w, stride, _, _ = B.symtile_heap_info(self.handle)
         assert w == world and stride == self.stride
+        self.failed_barriers = 0     # barriers that reported ETIMEOUT or a stale workspace
 
     def close(self) -> None:
         if self.handle:
@@ -82,7 +83,17 @@ class Heap:
         return flat.as_strided([self.world, *shape], strides, base)
 
     def barrier(self, stream: int | None = None) -> None:
-        B.symtile_barrier(self.handle, current_stream() if stream is None else stream)
+        """symtile_barrier.  A reported timeout or stale split-K workspace
+        bumps ``failed_barriers``, so the GatheredOutput objects of this heap
+        zero their split-K workspaces before their next split-K call (the
+        barrier has drained the stream, so no slice of the failed call is
+        still running)."""
+        try:
+            B.symtile_barrier(self.handle, current_stream() if stream is None else stream)
+        except B.SymtileError as e:
+            if e.name in ("ETIMEOUT", "EINVAL"):
+                self.failed_barriers += 1
+            raise
 
     def fill(self, rank: int, offset: int, nbytes: int, value: int,
              stream: int | None = None) -> None:
@@ -114,6 +125,7 @@ class GatheredOutput:
                                  device=heap.mem.device)
         self.ready_epoch = 0     # value of every ready counter after the last WG_SPEC call
         self.ws = None           # split-K workspace (uint8 device tensor), grown on demand
+        self.ws_seen = heap.failed_barriers   # failed barriers already answered by a reset
 
     def C(self, rank: int) -> torch.Tensor:
         return self.heap.view(rank, self.c_off, (self.M, self.heap.world * self.N_local),
@@ -142,6 +154,9 @@ class GatheredOutput:
         if self.ws is None or self.ws.numel() < need:
             self.ws = None
             self.ws = torch.zeros(need, dtype=torch.uint8, device=self.heap.mem.device)
+        elif self.ws_seen != self.heap.failed_barriers:
+            self.ws.zero_()      # a timed-out call may have left its counters non-zero
+        self.ws_seen = self.heap.failed_barriers
         return self.ws
 
     def reset_workspace(self) -> None:

@@ -4,6 +4,8 @@ Expected values come from ``oracle`` only; the HIP path is reached through
 the package's C-ABI binding."""
 from __future__ import annotations
 
+from typing import NamedTuple
+
 import numpy as np
 import pytest
 import torch
@@ -71,14 +73,61 @@ def oracle_block(A: torch.Tensor, B: torch.Tensor, dtype: str) -> np.ndarray:
                        oracle.decode16(workload.bits(B), dtype))
 
 
-def check_block(got16: np.ndarray, want32: np.ndarray, dtype: str, what: str = ""):
-    """Values of one rank block: finite, within tol * max|C|."""
+class BoundedBlock(NamedTuple):
+    """An oracle block with what the per-element accumulation bound needs:
+    c = A @ B and abs_ab = |A| @ |B| (both by the oracle, fp32), and K."""
+    c: np.ndarray
+    abs_ab: np.ndarray
+    K: int
+
+
+def oracle_block_bounded(A: torch.Tensor, B: torch.Tensor, dtype: str) -> BoundedBlock:
+    a = oracle.decode16(workload.bits(A), dtype)
+    b = oracle.decode16(workload.bits(B), dtype)
+    return BoundedBlock(oracle.gemm(a, b), oracle.gemm(np.abs(a), np.abs(b)), int(a.shape[1]))
+
+
+# precision (significand bits, implicit bit included) and least normal exponent
+_FMT = {"bf16": (8, -126), "f16": (11, -14)}
+
+
+def accumulation_bound_violations(got: np.ndarray, ref: np.ndarray, abs_ab: np.ndarray, K: int,
+                                  dtype: str) -> np.ndarray:
+    """Mask of elements where |got - ref| exceeds the error analysis of the
+    computation: got is an fp32 accumulation of K products rounded once to
+    the output format, ref the oracle's fp32 accumulation of the same
+    products.  Each fp32 sum of K terms lies within gamma_K * sum|a||b| of
+    the exact value (gamma_K = K u / (1 - K u), u = 2^-24, whatever the
+    order), and the output rounding adds at most half an output ulp of the
+    value (taken at the larger of |got| and |ref|, which bounds it from
+    above), so |got - ref| <= half_ulp + 2 gamma_K (|A||B|)_ij."""
+    p, emin = _FMT[dtype]
+    u = 2.0 ** -24
+    gamma = K * u / (1.0 - K * u)
+    mag = np.maximum(np.abs(got), np.abs(ref)).astype(np.float64)
+    with np.errstate(divide="ignore"):
+        e = np.where(mag > 0, np.floor(np.log2(np.where(mag > 0, mag, 1.0))), emin)
+    half_ulp = np.exp2(np.maximum(e, emin) - p)
+    bound = half_ulp + 2.0 * gamma * abs_ab.astype(np.float64)
+    return np.abs(got.astype(np.float64) - ref.astype(np.float64)) > bound
+
+
+def check_block(got16: np.ndarray, want, dtype: str, what: str = ""):
+    """Values of one rank block: finite, within tol * max|C| (the stated
+    tolerance); for a BoundedBlock also every element within the per-element
+    accumulation bound."""
     got = torch.from_numpy(got16.view(np.int16).copy()).view(tdtype(dtype)).float().numpy()
+    want32 = want.c if isinstance(want, BoundedBlock) else want
     assert np.all(np.isfinite(got)), f"{what}: non-finite (unwritten or overflow) elements"
     scale = float(np.max(np.abs(want32))) if want32.size else 0.0
     err = float(np.max(np.abs(got.astype(np.float64) - want32))) if want32.size else 0.0
     assert err <= TOL[dtype] * max(scale, 1e-30), \
         f"{what}: max|err| {err:.3e} > {TOL[dtype]} * max|C| {scale:.3e}"
+    if isinstance(want, BoundedBlock) and want32.size:
+        bad = accumulation_bound_violations(got, want.c, want.abs_ab, want.K, dtype)
+        assert not bad.any(), \
+            f"{what}: {int(bad.sum())} elements outside the accumulation bound, first at " \
+            f"{tuple(int(i) for i in np.argwhere(bad)[0])}"
     return err, scale
 
 

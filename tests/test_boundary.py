@@ -9,6 +9,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "symtile.h")
+DEVICE_HEADER = os.path.join(ROOT, "include", "symtile_device.h")
 PKG = os.path.join(ROOT, "paper_2511_12500_amd")
 LIB = os.path.join(PKG, "libsymtile.so")
 
@@ -33,6 +34,25 @@ def test_header_declares_the_boundary():
                      "symtile_gemm_all_scatter", "symtile_tile_copy", "symtile_barrier",
                      "symtile_atomic_exercise", "symtile_heap_bases"):
         assert required in names
+
+
+def test_device_api_header_is_part_of_the_boundary():
+    """The device-side API (Section 3.3 device API table) is the header-only
+    include/symtile_device.h: translate, value load/store, tile put/get/copy,
+    the eight atomics with ordering and scope, and the per-tile flag verbs;
+    every kernel source of the library includes it from there (no private
+    copy under the package)."""
+    assert os.path.exists(DEVICE_HEADER)
+    text = open(DEVICE_HEADER).read()
+    for verb in ("translate", "load", "store", "put", "get", "copy", "atomic_add", "atomic_xchg",
+                 "atomic_cas", "atomic_and", "atomic_or", "atomic_xor", "atomic_min",
+                 "atomic_max", "flag_publish", "flag_wait"):
+        assert re.search(r"__device__ __forceinline__ [\w:<>* ]+\b%s\(" % verb, text), verb
+    csrc = os.path.join(PKG, "csrc")
+    assert not os.path.exists(os.path.join(csrc, "symtile_device.h"))
+    from paper_2511_12500_amd.build import SOURCES
+    for src in SOURCES:
+        assert '#include "symtile_device.h"' in open(os.path.join(csrc, src)).read(), src
 
 
 def test_library_exports_every_declared_symbol(libpath):

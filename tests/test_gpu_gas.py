@@ -9,7 +9,7 @@ import torch
 import oracle
 import workload
 from tests.gpu_util import (SENTINEL, Problem, check_block, check_gathered, oracle_block,
-                            require_gpu, sym, u16)
+                            oracle_block_bounded, require_gpu, sym, u16)
 
 pytestmark = pytest.mark.gpu
 
@@ -26,7 +26,8 @@ def _gpu():
 
 
 def _blocks(p):
-    return {r: oracle_block(p.A, p.shards[r], p.dtype) for r in range(p.world)}
+    """Oracle blocks of every rank, with the per-element accumulation bound."""
+    return {r: oracle_block_bounded(p.A, p.shards[r], p.dtype) for r in range(p.world)}
 
 
 # ---------------------------------------------------------------- tiny two-rank case
@@ -179,7 +180,7 @@ def test_k_zero_with_split_k():
 def test_small_bf16_w8_rank0(variant):
     w = workload.SMALL_BF16
     p = Problem(w.world, w.M, w.N_local, w.K, w.dtype, w.tile_m, w.tile_n, dist=w.dist)
-    want = {0: oracle_block(p.A, p.shards[0], w.dtype)}
+    want = {0: oracle_block_bounded(p.A, p.shards[0], w.dtype)}
     p.sentinel()
     p.run(0, variant)
     p.barrier()
@@ -384,11 +385,95 @@ def test_argument_errors():
     with pytest.raises(pkg.SymtileError) as e:
         call(c0, f0, dtype=pkg.F32)
     assert e.value.name == "EUNSUPPORTED"
+    with pytest.raises(pkg.SymtileError) as e:           # 256x256 is built with 8 waves only
+        call(c0, f0, cfg=pkg.GasConfig(variant=FUSED, tile_m=256, tile_n=256, waves_per_wg=4))
+    assert e.value.name == "EUNSUPPORTED"
     p.heap.barrier()
 
 
-@pytest.mark.parametrize("case", [(8, 1024, 1024, 4096, 256, 256, "bf16"),
-                                  (3, 300, 264, 200, 256, 256, "f16"),
+def test_padded_strides_on_tightly_sized_buffers():
+    """lda > K and ldb > N_local through the C ABI, with A and B in buffers
+    that end exactly at their last element and NaN in every padding element:
+    the padding is never read into a stored value (any NaN would show), and
+    the result matches the oracle."""
+    pkg = sym()
+    world, rank, M, N, K, lda, ldb = 3, 1, 300, 136, 200, 264, 200
+    for tm, tn in ((128, 128), (256, 256), (64, 64)):
+        p = Problem(world, M, N, K, "bf16", tm, tn, seed=21)
+        bf = torch.bfloat16
+        a_buf = torch.full(((M - 1) * lda + K,), float("nan"), dtype=bf, device="cuda")
+        b_buf = torch.full(((K - 1) * ldb + N,), float("nan"), dtype=bf, device="cuda")
+        a_buf.as_strided((M, K), (lda, 1)).copy_(p.dA)
+        b_buf.as_strided((K, N), (ldb, 1)).copy_(p.dB[rank])
+        p.sentinel()
+        for variant in (FUSED, BULK):
+            pkg.symtile_gemm_all_scatter(
+                p.heap.handle, a_buf.data_ptr(), b_buf.data_ptr(), p.heap.ptr(rank, p.out.c_off),
+                p.heap.ptr(rank, p.out.flag_off), p.out.ready.data_ptr(), M, N, K, lda, ldb,
+                pkg.BF16, rank, world, pkg.GasConfig(variant=variant, tile_m=tm, tile_n=tn),
+                pkg.current_stream())
+            p.calls[rank] += 1
+            p.barrier()
+            check_gathered(p, {rank: oracle_block_bounded(p.A, p.shards[rank], "bf16")})
+
+
+def test_split_k_timeout_then_stale_workspace_is_reported():
+    """A reducing slice allowed one poll gives up on the tiles whose partner
+    partial is not yet counted (ETIMEOUT at the barrier) and leaves their
+    counters as they are.  A later call on the same workspace, made without
+    zeroing it, reports the stale counters (EINVAL at the barrier) and writes
+    no stale sum; the Python wrapper zeroes the workspace after either report,
+    and its next call is exact."""
+    pkg = sym()
+    world, rank = 2, 0
+    p = Problem(world, 1024, 512, 2048, "bf16", 64, 64, seed=17)     # 128 tiles x 2 slices
+    want = {rank: oracle_block_bounded(p.A, p.shards[rank], "bf16")}
+    p.sentinel()
+    p.run(rank, FUSED, split_k=2, spin_limit=1)
+    try:
+        p.heap.barrier()
+        timed_out = False
+    except pkg.SymtileError as e:
+        assert e.name == "ETIMEOUT", e
+        timed_out = True
+    torch.cuda.synchronize()
+    if not timed_out:                        # every partner was early: an ordinary call
+        check_gathered(p, want)
+        assert np.all(_ws_counters(p) == 0)
+    else:
+        stale = _ws_counters(p).reshape(-1, 2)
+        assert np.any(stale[:, 0] != 0)      # tickets left behind by the timed-out tiles
+        assert np.all((stale[:, 0] == 0) | (stale[:, 0] == 2))
+        # the same workspace again, through the C ABI (no reset)
+        ws = p.out.ws
+        p.out.C_all().view(torch.int16).fill_(-1)
+        pkg.symtile_gemm_all_scatter(
+            p.heap.handle, p.dA.data_ptr(), p.dB[rank].data_ptr(), p.heap.ptr(rank, p.out.c_off),
+            p.heap.ptr(rank, p.out.flag_off), p.out.ready.data_ptr(), p.M, p.N, p.K, p.K, p.N,
+            pkg.BF16, rank, world,
+            pkg.GasConfig(variant=FUSED, tile_m=64, tile_n=64, split_k=2,
+                          workspace=ws.data_ptr(), workspace_bytes=ws.numel()),
+            pkg.current_stream())
+        with pytest.raises(pkg.SymtileError) as e:
+            p.heap.barrier()
+        assert e.value.name == "EINVAL" and "workspace" in str(e.value)
+        torch.cuda.synchronize()
+        G = u16(p.out.C_all())[0][:, :p.N].reshape(16, 64, 8, 64)
+        tm, tn = np.nonzero(stale[:, 0].reshape(16, 8))
+        for m, n in zip(tm, tn):             # a stale tile is left unwritten
+            assert np.all(G[m, :, n, :] == SENTINEL), (m, n)
+    # the wrapper zeroes the workspace after a failed barrier: exact again
+    p.sentinel()
+    p.calls[:] = 0
+    p.out.arrived_all().zero_()
+    p.run(rank, FUSED, split_k=2)
+    p.barrier()
+    check_gathered(p, want)
+    assert np.all(_ws_counters(p) == 0)
+
+
+@pytest.mark.parametrize("case", [(8, 1024, 1024, 4096, 256, 128, "bf16"),
+                                  (3, 300, 264, 200, 256, 128, "f16"),
                                   (2, 512, 256, 320, 256, 128, "bf16"),
                                   (4, 300, 264, 200, 128, 128, "bf16"),
                                   (8, 1024, 1024, 4096, 128, 128, "f16")],
@@ -594,13 +679,19 @@ def test_split_k_two_slices_match_one_within_rounding():
     check_block(u16(p.out.C(0)[:, :256]), oracle_block(p.A, p.shards[0], "bf16"), "bf16")
 
 
-@pytest.mark.parametrize("wl", [workload.WIDE_F16, workload.SMALL_BF16], ids=lambda w: w.name)
-def test_split_k_full_size_matches_oracle(wl):
-    """The full-size shapes with few 256x256 tiles (128 and 16), split so
-    every CU has a slice, in the configuration the benchmark runs."""
-    split = 2 if wl is workload.WIDE_F16 else 16
-    p = _large_case(wl, seed=4)
-    want = {0: oracle_block(p.A, p.shards[0], wl.dtype)}
+@pytest.mark.parametrize("wl,tile,split",
+                         [(workload.WIDE_F16, 256, 2), (workload.SMALL_BF16, 256, 16),
+                          (workload.SMALL_BF16, 128, 4)],
+                         ids=lambda x: getattr(x, "name", str(x)))
+def test_split_k_full_size_matches_oracle(wl, tile, split):
+    """The full-size shapes with few tiles, split so every CU has a slice:
+    fp16 8192x8192.8192x1024 with 256x256 tiles in 2 slices and bf16
+    1024x4096.4096x1024 with 128x128 tiles (8 waves) in 4 slices, the
+    configurations the benchmark runs, and the latter with 256x256 tiles in
+    16 slices."""
+    p = Problem(wl.world, wl.M, wl.N_local, wl.K, wl.dtype, tile, tile, dist=wl.dist, seed=4)
+    want = {0: (oracle_block_bounded if wl.M * wl.N_local <= 1 << 22 else oracle_block)(
+        p.A, p.shards[0], wl.dtype)}
     p.sentinel()
     p.run(0, FUSED, split_k=split, nontemporal=2)
     p.barrier()
@@ -684,7 +775,7 @@ def _random_cases(n=64, seed=2027):
         variant = variants[rng.randint(len(variants))]
         waves = 0
         if (tm, tn) in ((256, 128), (256, 256)) and variant != WAVESPEC and rng.rand() < 0.3:
-            waves = 4
+            waves = 4 if (tm, tn) == (256, 128) else 0   # 256x256 is built with 8 waves only
         split = 0
         stages = -(-K // 32)
         if variant in (BULK, FUSED) and stages > 1 and rng.rand() < 0.5:
@@ -699,7 +790,7 @@ def _random_cases(n=64, seed=2027):
 def test_random_calls_match_oracle(case):
     world, M, N, K, tm, tn, dtype, variant, waves, split, rank = case
     p = Problem(world, M, N, K, dtype, tm, tn, seed=M + N + K)
-    want = {rank: oracle_block(p.A, p.shards[rank], dtype)}
+    want = {rank: oracle_block_bounded(p.A, p.shards[rank], dtype)}
     p.sentinel()
     p.run(rank, variant, waves_per_wg=waves, split_k=split)
     p.barrier()

@@ -121,3 +121,130 @@ def test_model_finds_a_planted_protocol_error():
     # increments (whichever interleaving the search reaches first)
     with pytest.raises(AssertionError, match="unwritten partial|counters left"):
         _explore(1, 2, 2, 2, wait_target=0)
+
+
+# ---------------------------------------------------------------------------
+# Timeouts.  A reducer whose bounded wait expires records ETIMEOUT and gives
+# the tile up without resetting its counters, because slices of that call
+# that already hold a ticket may still count themselves afterwards.  A later
+# call on the same workspace then draws tickets at or past S for that tile,
+# and each such slice reports a stale workspace and skips the tile instead
+# of taking part (and instead of a reducer summing partials that were never
+# written in that call).
+
+def _run_call(T, S, G, R, cnt0, written0, allow_timeout, reset_on_timeout, check_tickets):
+    """Every interleaving of one call starting from counters cnt0/written0.
+    Returns the set of end states (cnt, written, reduced, flagged, timed_out)."""
+    units = [[u for u in range(g, T * S, G)] for g in range(G)]
+    ends = set()
+    seen = set()
+
+    def explore(state):
+        if state in seen:
+            return
+        seen.add(state)
+        wgs, resident, cnt, written, parts, reduced, flagged, timed = state
+        if all(i == len(units[g]) for g, (i, _, _) in enumerate(wgs)):
+            ends.add((cnt, written, reduced, flagged, timed))
+            return
+        moves = []
+        if len(resident) < R:
+            for g in range(G):
+                if g not in resident and wgs[g][0] == 0 and wgs[g][1] == START and units[g]:
+                    moves.append(("admit", g))
+        for g in resident:
+            i, pc, _ = wgs[g]
+            t, _s = divmod(units[g][i], S)
+            if pc == WAIT and written[t] < S - 1:
+                if allow_timeout:
+                    moves.append(("timeout", g))
+                continue
+            moves.append(("step", g))
+        assert moves, f"deadlock in {state}"
+        for kind, g in moves:
+            w, res = list(wgs), list(resident)
+            c, wr, pa = list(cnt), list(written), list(parts)
+            rd, fl, tm = list(reduced), list(flagged), list(timed)
+            if kind == "admit":
+                res.append(g)
+                explore((tuple(w), tuple(res), tuple(c), tuple(wr), tuple(pa), tuple(rd),
+                         tuple(fl), tuple(tm)))
+                continue
+            i, pc, ticket = w[g]
+            t, s = divmod(units[g][i], S)
+            if kind == "timeout":
+                tm[t] += 1
+                if reset_on_timeout:
+                    c[t] = wr[t] = 0
+                pc = DONE
+            elif pc == START:
+                ticket = c[t]
+                c[t] += 1
+                if check_tickets and ticket >= S:
+                    fl[t] += 1                             # stale workspace: skip the tile
+                    pc = DONE
+                else:
+                    pc = WAIT if ticket + 1 == S else WRITE
+            elif pc == WRITE:
+                pa[t] |= 1 << s
+                pc = COUNT
+            elif pc == COUNT:
+                wr[t] += 1
+                pc = DONE
+            elif pc == WAIT:
+                pc = READ
+            elif pc == READ:
+                others = ((1 << S) - 1) & ~(1 << s)
+                assert pa[t] & others == others, "reducer read an unwritten partial"
+                pc = RESET
+            elif pc == RESET:
+                c[t] = wr[t] = 0
+                rd[t] += 1
+                pc = DONE
+            if pc == DONE:
+                i, pc, ticket = i + 1, START, 0
+                if i == len(units[g]):
+                    res.remove(g)
+            w[g] = (i, pc, ticket)
+            explore((tuple(w), tuple(res), tuple(c), tuple(wr), tuple(pa), tuple(rd),
+                     tuple(fl), tuple(tm)))
+
+    explore((tuple((0, START, 0) for _ in range(G)), (), tuple(cnt0), tuple(written0),
+             (0,) * T, (0,) * T, (0,) * T, (0,) * T))
+    return ends
+
+
+def _timeout_then_next_call(T, S, G, R, reset_on_timeout=False, check_tickets=True):
+    zero = (0,) * T
+    first = _run_call(T, S, G, R, zero, zero, True, reset_on_timeout, check_tickets)
+    assert any(any(tm) for *_, tm in first), "the model never timed out"
+    for cnt, written, reduced, flagged, timed in first:
+        for t in range(T):
+            # each tile of the first call is reduced once, or given up by a timeout
+            assert reduced[t] + timed[t] == 1 and flagged[t] == 0, (reduced, timed)
+        second = _run_call(T, S, G, R, cnt, written, False, reset_on_timeout, check_tickets)
+        for _, _, reduced2, flagged2, _ in second:
+            for t in range(T):
+                clean = cnt[t] == 0 and written[t] == 0
+                if clean:
+                    assert reduced2[t] == 1 and flagged2[t] == 0, "clean tile not reduced once"
+                else:
+                    # every slice reports the stale workspace; nothing is summed
+                    assert reduced2[t] == 0 and flagged2[t] == S, \
+                        f"stale tile neither reduced nor reported ({reduced2}, {flagged2})"
+
+
+@pytest.mark.parametrize("T,S,G,R", [(1, 2, 2, 2), (1, 3, 3, 2), (2, 2, 2, 2), (2, 2, 4, 2)])
+def test_split_k_timeout_leaves_counters_and_the_next_call_reports_them(T, S, G, R):
+    _timeout_then_next_call(T, S, G, R)
+
+
+def test_timeout_model_finds_the_planted_errors():
+    """Pins of the timeout model: resetting the counters on the timeout path
+    lets a late arrival's count survive into the next call, whose reducer then
+    passes its wait before its partner's partial is written; without the
+    ticket check a stale tile is silently never written."""
+    with pytest.raises(AssertionError, match="unwritten partial"):
+        _timeout_then_next_call(1, 2, 2, 2, reset_on_timeout=True)
+    with pytest.raises(AssertionError, match="neither reduced nor reported"):
+        _timeout_then_next_call(1, 2, 2, 2, check_tickets=False)
