@@ -377,6 +377,38 @@ symtile_status symtile_gemm_all_scatter(symtile_heap* h, const void* A, const vo
                                         int ldb, int dtype, int rank, int world_size,
                                         const symtile_gas_config* cfg, symtile_stream s);
 
+/* Bytes of the scratch behind symtile_gemm_all_scatter_noalloc: 64 MiB of
+ * fp32 partial tiles plus 64 KiB of tile counters (the split-K workspace of
+ * the fp16 8192x8192 x 8192x1024 problem with 256x256 tiles in 2 K slices
+ * fits). */
+#define SYMTILE_NOALLOC_SCRATCH_BYTES ((64u << 20) + (64u << 10))
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the same call as
+ * symtile_gemm_all_scatter, with the same arguments, results and errors, but
+ * the split-K workspace comes from a scratch array the library keeps in
+ * static device memory, SYMTILE_NOALLOC_SCRATCH_BYTES per GPU, held from the
+ * library's first use on that GPU until the process ends.  The call makes no
+ * hipMalloc or hipFree and calls no allocating library routine.
+ *  - cfg->workspace must be NULL and cfg->workspace_bytes 0 (EINVAL otherwise);
+ *  - a split_k > 1 call whose workspace (symtile_gas_workspace_bytes) exceeds
+ *    the scratch returns EINVAL and launches nothing;
+ *  - the scratch's counters are zeroed by a kernel at the start of every
+ *    split_k > 1 call (no memset node), so a timed-out earlier call leaves
+ *    nothing behind for the next one;
+ *  - UNFUSED_PC is EUNSUPPORTED (it creates a stream and events on first use);
+ *  - every call on one GPU shares that GPU's scratch: split_k > 1 calls that
+ *    overlap in time on one GPU (other streams, other threads) race and give
+ *    wrong results.  Calls on one stream are ordered and safe.
+ * The scratch's device address is looked up (hipGetSymbolAddress) on the
+ * first split_k > 1 call on each device. */
+symtile_status symtile_gemm_all_scatter_noalloc(symtile_heap* h, const void* A,
+                                                const void* B_shard, void* C_gathered_local,
+                                                uint32_t* arrived_local, uint32_t* ready, int M,
+                                                int N_local, int K, int lda, int ldb, int dtype,
+                                                int rank, int world_size,
+                                                const symtile_gas_config* cfg, symtile_stream s);
+
 /* Rate of the realtime counter behind trace timestamps, in kHz. */
 symtile_status symtile_clock_rate_khz(int device, int* khz);
 

@@ -14,7 +14,7 @@ _BINDING = (
     "TRACE_WORDS", "UNFUSED_PC", "WAVE_SPEC", "WG_SPEC", "GasConfig", "SymtileError", "lib", "symtile_atomic_exercise",
     "symtile_barrier", "symtile_clock_rate_khz", "symtile_device_info",
     "symtile_gas_workspace_bytes", "symtile_gemm_all_scatter",
-    "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
+    "symtile_gemm_all_scatter_noalloc", "NOALLOC_SCRATCH_BYTES", "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
     "symtile_heap_destroy", "symtile_heap_fill", "symtile_heap_info", "symtile_heap_ptr",
     "symtile_last_error", "symtile_tile_copy", "symtile_translate", "symtile_translate_device",
     "symtile_value_exercise", "symtile_version",

@@ -80,6 +80,8 @@ def _load():
                               vp],
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
+        "symtile_gemm_all_scatter_noalloc": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
+                                             i32, i32, i32, ctypes.POINTER(GasConfig), vp],
         "symtile_device_info": [i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)],
         "symtile_gas_workspace_bytes": [i32, i32, i32, i32, i32, ctypes.POINTER(sz)],
         "symtile_clock_rate_khz": [i32, ctypes.POINTER(i32)],
@@ -226,6 +228,23 @@ def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int
                                         dtype, rank, world_size,
                                         ctypes.byref(cfg) if cfg is not None else None,
                                         _vp(stream)), "symtile_gemm_all_scatter")
+
+
+NOALLOC_SCRATCH_BYTES = (64 << 20) + (64 << 10)   # SYMTILE_NOALLOC_SCRATCH_BYTES
+
+
+def symtile_gemm_all_scatter_noalloc(h: int, A: int, B_shard: int, C_gathered_local: int,
+                                     arrived_local: int, ready: int, M: int, N_local: int, K: int,
+                                     lda: int, ldb: int, dtype: int, rank: int, world_size: int,
+                                     cfg: GasConfig | None, stream: int = 0) -> None:
+    """symtile_gemm_all_scatter with the split-K workspace in the library's
+    static scratch (cfg.workspace must be None)."""
+    _check(lib.symtile_gemm_all_scatter_noalloc(_vp(h), _vp(A), _vp(B_shard),
+                                                _vp(C_gathered_local), _vp(arrived_local),
+                                                _vp(ready), M, N_local, K, lda, ldb, dtype, rank,
+                                                world_size,
+                                                ctypes.byref(cfg) if cfg is not None else None,
+                                                _vp(stream)), "symtile_gemm_all_scatter_noalloc")
 
 
 def symtile_gas_workspace_bytes(M: int, N_local: int, tile_m: int, tile_n: int,

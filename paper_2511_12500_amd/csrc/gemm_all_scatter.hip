@@ -41,6 +41,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <type_traits>
 
@@ -1053,6 +1054,44 @@ size_t sk_workspace_bytes(size_t tiles, int bm, int bn, int split) {
     return split <= 1 ? 0 : sk_counter_bytes(tiles) + tiles * split * (size_t)bm * bn * 4;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of the allocation-free entry point: the split-K workspace (tile
+// counters, then fp32 partial tiles) in a static device array, one copy per
+// GPU, held from the library's first use on that GPU until the process ends.
+// Host code never passes this name to a kernel or a copy (on the host it is
+// only a stand-in for the symbol): its device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) uint8_t g_noalloc_scratch[SYMTILE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+symtile_status noalloc_scratch(int device, void** out) {
+    if (device < 0 || device >= kMaxDevices)
+        return symtile_host::fail(SYMTILE_EINVAL, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        int prev = -1;
+        SYMTILE_HIP(hipGetDevice(&prev));
+        SYMTILE_HIP(hipSetDevice(device));
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_noalloc_scratch));
+        (void)hipSetDevice(prev);
+        if (e != hipSuccess) return symtile_host::hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return symtile_host::fail(SYMTILE_EHIP, "scratch symbol has no device address");
+        g_scratch_ptr[device] = ptr;
+    }
+    *out = g_scratch_ptr[device];
+    return SYMTILE_OK;
+}
+
+// Zero n 32-bit words (the split-K counters) with a kernel, so the call adds
+// no memset node when a caller captures it into a graph.
+__global__ __launch_bounds__(256) void zero_words_kernel(uint32_t* p, int n) {
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
 }  // namespace
 
 extern "C" symtile_status symtile_gas_workspace_bytes(int M, int N_local, int tile_m, int tile_n,
@@ -1295,4 +1334,53 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     void* args[] = {&p};
     SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g + c), dim3(64 * v->waves), args, 0, stream));
     return SYMTILE_OK;
+}
+
+extern "C" symtile_status symtile_gemm_all_scatter_noalloc(
+    symtile_heap* h, const void* A, const void* B_shard, void* C_gathered_local,
+    uint32_t* arrived_local, uint32_t* ready, int M, int N_local, int K, int lda, int ldb,
+    int dtype, int rank, int world_size, const symtile_gas_config* cfg_in, symtile_stream s) {
+    using symtile_host::fail;
+    if (!h) return fail(SYMTILE_EINVAL, "heap is NULL");
+    symtile_gas_config cfg{};
+    if (cfg_in) cfg = *cfg_in;
+    if (cfg.workspace || cfg.workspace_bytes)
+        return fail(SYMTILE_EINVAL, "the allocation-free call takes no workspace (it uses the "
+                                    "library's scratch)");
+    if (cfg.variant == SYMTILE_UNFUSED_PC)
+        return fail(SYMTILE_EUNSUPPORTED, "UNFUSED_PC creates a stream and events on first use; "
+                                          "the allocation-free call does not run it");
+    if (cfg.split_k <= 1)
+        return symtile_gemm_all_scatter(h, A, B_shard, C_gathered_local, arrived_local, ready, M,
+                                        N_local, K, lda, ldb, dtype, rank, world_size, &cfg, s);
+    if (cfg.tile_m == 0 && cfg.tile_n == 0) cfg.tile_m = cfg.tile_n = 256;
+    size_t need = 0;
+    if (symtile_status st =
+            symtile_gas_workspace_bytes(M, N_local, cfg.tile_m, cfg.tile_n, cfg.split_k, &need))
+        return st;
+    if (need > (size_t)SYMTILE_NOALLOC_SCRATCH_BYTES)
+        return fail(SYMTILE_EINVAL, "split-K workspace of " + std::to_string(need) +
+                                        " bytes exceeds the scratch of " +
+                                        std::to_string((size_t)SYMTILE_NOALLOC_SCRATCH_BYTES) +
+                                        " bytes");
+    if (need == 0)   // no tiles
+        return symtile_gemm_all_scatter(h, A, B_shard, C_gathered_local, arrived_local, ready, M,
+                                        N_local, K, lda, ldb, dtype, rank, world_size, &cfg, s);
+    void* scratch = nullptr;
+    if (symtile_status st = noalloc_scratch(h->device, &scratch)) return st;
+    // the counters start at zero on every call, whatever an earlier call left
+    const size_t tiles = (size_t)((M + cfg.tile_m - 1) / cfg.tile_m) *
+                         ((N_local + cfg.tile_n - 1) / cfg.tile_n);
+    const int words = (int)(sk_counter_bytes(tiles) / 4);
+    int prev = -1;
+    if (symtile_status st = symtile_host::set_device(h, &prev)) return st;
+    hipLaunchKernelGGL(zero_words_kernel, dim3(std::min((words + 255) / 256, 1024)), dim3(256), 0,
+                       static_cast<hipStream_t>(s), static_cast<uint32_t*>(scratch), words);
+    const hipError_t e = hipGetLastError();
+    (void)hipSetDevice(prev);
+    if (e != hipSuccess) return symtile_host::hip_fail(e, "zero_words_kernel launch");
+    cfg.workspace = scratch;
+    cfg.workspace_bytes = SYMTILE_NOALLOC_SCRATCH_BYTES;
+    return symtile_gemm_all_scatter(h, A, B_shard, C_gathered_local, arrived_local, ready, M,
+                                    N_local, K, lda, ldb, dtype, rank, world_size, &cfg, s);
 }
