@@ -166,10 +166,13 @@ symtile_status symtile_heap_destroy(symtile_heap* h);
 symtile_status symtile_heap_alloc(symtile_heap* h, size_t bytes, size_t align,
                                   size_t* offset_out);
 
-/* Device address of `offset` in slot `rank`. */
+/* Device address of `offset` in slot `rank`: the symmetric object at that
+ * offset as rank `rank` holds it (Section 3.2.3, tensors in the symmetric
+ * heap).  EINVAL for a bad rank or an offset past the slot. */
 symtile_status symtile_heap_ptr(const symtile_heap* h, int rank, size_t offset, void** out);
 
-/* Heap geometry: world size, slot stride, bytes allocated per slot, device. */
+/* Heap geometry (Section 3.2.1, get_num_ranks): world size, slot stride,
+ * bytes allocated per slot, device.  Any output may be NULL. */
 symtile_status symtile_heap_info(const symtile_heap* h, int* world_size, size_t* slot_stride,
                                  size_t* used, int* device);
 
@@ -185,9 +188,9 @@ symtile_status symtile_heap_bases(const symtile_heap* h, const uint64_t** dev_ba
 symtile_status symtile_translate(const symtile_heap* h, const void* p, int from_rank,
                                  int to_rank, void** out);
 
-/* Device translation applied to n addresses: out[i] = translate(in[i],
- * from_rank, to_rank) computed by a kernel with the same device routine the
- * hot path uses.  in and out are device arrays of n uint64.  Addresses are
+/* Device translation (Section 3.3.1) applied to n addresses: out[i] =
+ * translate(in[i], from_rank, to_rank) computed by a kernel with the same
+ * device routine the hot path uses.  in and out are device arrays of n uint64.  Addresses are
  * not range-checked on the device (the caller checks with the host twin). */
 symtile_status symtile_translate_device(const symtile_heap* h, const uint64_t* in, int n,
                                         int from_rank, int to_rank, uint64_t* out,
@@ -201,8 +204,9 @@ symtile_status symtile_translate_device(const symtile_heap* h, const uint64_t* i
 symtile_status symtile_barrier(symtile_heap* h, symtile_stream s);
 
 /* Fill `bytes` at `offset` of slot `rank` (every slot when rank < 0) with
- * the byte `value`, with a fill kernel on stream s (no memset node, so it
- * may be captured into a graph). */
+ * the byte `value` (Section 3.2.3, tensor creation: zeros / full in the
+ * symmetric heap), with a fill kernel on stream s (no memset node, so it may
+ * be captured into a graph).  EINVAL for a bad rank or a range past the slot. */
 symtile_status symtile_heap_fill(symtile_heap* h, int rank, size_t offset, size_t bytes,
                                  int value, symtile_stream s);
 
@@ -329,7 +333,10 @@ symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off
 /* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
 
 /* Bytes of the split-K workspace (symtile_gas_config.workspace) of a call
- * with this output shape, tile and split_k: two uint32 counters per tile
+ * with this output shape, tile and split_k.  Splitting the K loop of the GEMM
+ * main-loop listing (Section 4) is this library's addition for shapes with
+ * fewer output tiles than CUs; the slices meet through this workspace: two
+ * uint32 counters per tile
  * (rounded up to 256 bytes), then split_k fp32 partial tiles of
  * tile_m * tile_n values per tile.  *bytes = 0 when split_k <= 1.  EINVAL for
  * negative sizes, a tile shape that is not built (see tile_m, tile_n above)
@@ -409,18 +416,23 @@ symtile_status symtile_gemm_all_scatter_noalloc(symtile_heap* h, const void* A,
                                                 int rank, int world_size,
                                                 const symtile_gas_config* cfg, symtile_stream s);
 
-/* Rate of the realtime counter behind trace timestamps, in kHz. */
+/* Rate of the realtime counter behind trace timestamps (the per-tile
+ * timeline of Section 3.4, instrumentation), in kHz.  EINVAL for a bad device
+ * or NULL khz. */
 symtile_status symtile_clock_rate_khz(int device, int* khz);
 
 /* Number of compute units of `device` and the largest WG_SPEC grid
- * (gemm_wgs + copy_wgs) that is co-resident for the given tile shape. */
+ * (gemm_wgs + copy_wgs) that is co-resident for the given tile shape: the
+ * budget the workgroup-specialised schedule splits between producers and
+ * consumers (Section 4.2.2).  EUNSUPPORTED for a tile shape not built. */
 symtile_status symtile_device_info(int device, int tile_m, int tile_n, int* cu_count,
                                    int* max_coresident_wgs);
 
-/* Thread-local message of the last failure in this thread ("" if none). */
+/* Thread-local message of the last failure in this thread ("" if none); the
+ * error channel of this C ABI, which the paper's Python API does not need. */
 const char* symtile_last_error(void);
 
-/* Library version string. */
+/* Library version string (names the GPU target). */
 const char* symtile_version(void);
 
 #ifdef __cplusplus

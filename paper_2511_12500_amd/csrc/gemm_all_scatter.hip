@@ -59,7 +59,6 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
 constexpr int BK = 32;                 // K depth of one pipeline stage
 constexpr int kRowBytes = BK * 2;      // LDS bytes per staged A row (4 chunks of 16 B)
 constexpr int NS = 4;                  // pipeline stages (LDS ring)
@@ -952,30 +951,32 @@ void gas_kernel(const GasParams p) {
     }
 }
 
+// Copy kernels of the bulk-synchronous and unfused producer-consumer
+// schedules run on CUs of their own, so their workgroups are wide (16 waves
+// keep many loads and stores in flight per CU).
+template <int BM>
+constexpr int copy_threads() { return BM >= 128 ? 1024 : 256; }
+
 // Second kernel of the bulk-synchronous schedule (Section 4.1.1).
 template <int BM, int BN>
-__global__ __launch_bounds__(kThreads) void scatter_kernel(const GasParams p) {
+__global__ __launch_bounds__(copy_threads<BM>()) void scatter_kernel(const GasParams p) {
     for (int t = blockIdx.x; t < p.num_tiles; t += gridDim.x) {
         const int tm = t / p.tiles_n, tn = t % p.tiles_n;
         uint64_t* tr = tile_trace(p, tm, tn);
         if (tr && threadIdx.x == 0)
             tr[SYMTILE_TRACE_COPY_WAIT] = tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
         with_store_policy(p.nontemporal, [&](auto pol) {
-            put_tile_to_peers<BM, BN, kThreads, decltype(pol)::value>(p, tm, tn);
+            put_tile_to_peers<BM, BN, copy_threads<BM>(), decltype(pol)::value>(p, tm, tn);
         });
         if (tr && threadIdx.x == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
     }
 }
 
 // Copy kernel of the unfused producer-consumer schedule (Section 4.1.2):
-// runs on its own stream next to the producer grid of gas_kernel, on CUs of
-// its own, so its workgroups are wide (16 waves keep many stores in flight).
-template <int BM>
-constexpr int consumer_threads() { return BM >= 128 ? 1024 : 256; }
-
+// runs on its own stream next to the producer grid of gas_kernel.
 template <int BM, int BN>
-__global__ __launch_bounds__(consumer_threads<BM>()) void consumer_kernel(const GasParams p) {
-    consume_tiles<BM, BN, consumer_threads<BM>()>(p, blockIdx.x, gridDim.x);
+__global__ __launch_bounds__(copy_threads<BM>()) void consumer_kernel(const GasParams p) {
+    consume_tiles<BM, BN, copy_threads<BM>()>(p, blockIdx.x, gridDim.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -986,7 +987,7 @@ struct Variant {
     const void* gas;
     const void* scatter;
     const void* consumer;
-    int consumer_threads;
+    int copy_threads;            // workgroup size of scatter_kernel and consumer_kernel
     const void* gas_ws;          // wave-specialised kernel (NW compute waves + 1), or null
 };
 
@@ -1005,7 +1006,7 @@ Variant make_variant() {
                    reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF>),
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>),
                    reinterpret_cast<const void*>(&consumer_kernel<BM, BN>),
-                   consumer_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>()};
+                   copy_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>()};
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
@@ -1266,7 +1267,7 @@ extern "C" symtile_status symtile_gemm_all_scatter(
             int c = cfg.copy_wgs > 0 ? cfg.copy_wgs : cus;
             c = std::min(c, ntiles);
             p.copy_wgs = c;
-            SYMTILE_HIP(hipLaunchKernel(v->scatter, dim3(c), dim3(kThreads), args, 0, stream));
+            SYMTILE_HIP(hipLaunchKernel(v->scatter, dim3(c), dim3(v->copy_threads), args, 0, stream));
         }
         return SYMTILE_OK;
     }
@@ -1312,7 +1313,7 @@ extern "C" symtile_status symtile_gemm_all_scatter(
         SYMTILE_HIP(hipEventRecord(h->ev_fork, stream));
         SYMTILE_HIP(hipStreamWaitEvent(cs, h->ev_fork, 0));
         SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(64 * v->waves), args, 0, stream));
-        SYMTILE_HIP(hipLaunchKernel(v->consumer, dim3(p.copy_wgs), dim3(v->consumer_threads),
+        SYMTILE_HIP(hipLaunchKernel(v->consumer, dim3(p.copy_wgs), dim3(v->copy_threads),
                                     args, 0, cs));
         SYMTILE_HIP(hipEventRecord(h->ev_join, cs));
         SYMTILE_HIP(hipStreamWaitEvent(stream, h->ev_join, 0));
