@@ -347,9 +347,12 @@ def bench_copy(args, torch, sym, workload, tile=None):
                               wl.shift, -1, flags, tiles_per_wg=args.copy_per_wg, stream=stream)
 
     st = settle(launch, torch, args)
-    # warm launches back to back, then the cold ones, each after the flush;
-    # the cold launches are the last copy-iters dispatches of the kernel (the
-    # committed rocprofv3 summary averages exactly those)
+    # warm launches back to back (an event pair each), then cold ones, each
+    # after the flush: first with an event pair around the launch (it holds
+    # the dispatch and the kernel-end fence, ~3 us), then -- the measurement --
+    # with events that bracket exactly the kernel (symtile_tile_copy_timed);
+    # these are the last copy-iters dispatches of the kernel, which the
+    # committed rocprofv3 summary averages
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.copy_iters)]
     for a, b in evs:
@@ -358,7 +361,7 @@ def bench_copy(args, torch, sym, workload, tile=None):
         b.record()
     torch.cuda.synchronize()
     warm = [a.elapsed_time(b) for a, b in evs]
-    cold = []
+    cold_launch = []
     for i in range(args.copy_iters):
         flush.max()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -366,12 +369,19 @@ def bench_copy(args, torch, sym, workload, tile=None):
         launch()
         b.record()
         torch.cuda.synchronize()
-        cold.append(a.elapsed_time(b))
+        cold_launch.append(a.elapsed_time(b))
+    cold = []
+    for i in range(args.copy_iters):
+        flush.max()
+        cold.append(sym.symtile_tile_copy_timed(heap.handle, src, dst, wl.rows, wl.cols, wl.cols,
+                                                sym.F32, t, t, wl.shift, -1, flags,
+                                                tiles_per_wg=args.copy_per_wg, stream=stream))
     heap.barrier()
     moved = wl.bytes_moved
-    # median of the individually timed cold launches (the mean is kept beside it)
+    # medians of the individually timed cold launches (the mean is kept beside it)
     cold_ms = statistics.median(cold)
     cold_mean_ms = statistics.fmean(cold)
+    cold_launch_ms = statistics.median(cold_launch)
     warm_ms = sum(warm) / len(warm)
     gbs = moved / (cold_ms * 1e-3) / 1e9
     prof = copy_profile_name(args, wl, t)
@@ -382,6 +392,8 @@ def bench_copy(args, torch, sym, workload, tile=None):
         "value": gbs, "unit": "GB/s", "tile": f"{t}x{t}", "workload": wl.name,
         "tiles_per_wg": args.copy_per_wg, "settle": st,
         "bytes_per_launch": moved, "cold_ms": cold_ms, "cold_mean_ms": cold_mean_ms,
+        "cold_launch_ms": cold_launch_ms,
+        "cold_launch_GBps": moved / (cold_launch_ms * 1e-3) / 1e9,
         "warm_ms": warm_ms,
         "warm_GBps": moved / (warm_ms * 1e-3) / 1e9,
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -330,6 +330,21 @@ symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off
                                  int shift, int only_rank, size_t flag_off, int tiles_per_wg,
                                  int mode, symtile_stream s);
 
+/* symtile_tile_copy launched with hipExtLaunchKernel, which records two
+ * events as part of the kernel's own dispatch instead of as separate marker
+ * packets around it, for measurement: the call waits for the kernel and
+ * *kernel_ms receives the elapsed time between the events in milliseconds
+ * (0 when nothing is launched): the kernel's duration plus less dispatch
+ * overhead than a pair of stream events around the launch holds.  The
+ * result in the heap is the same as symtile_tile_copy's.  The events belong
+ * to the heap (created on first use).  Errors: those of symtile_tile_copy;
+ * EINVAL for a NULL kernel_ms; EHIP when the events cannot be created or read. */
+symtile_status symtile_tile_copy_timed(symtile_heap* h, size_t src_off, size_t dst_off, int rows,
+                                       int cols, int ld, int dtype, int tile_r, int tile_c,
+                                       int shift, int only_rank, size_t flag_off,
+                                       int tiles_per_wg, int mode, symtile_stream s,
+                                       float* kernel_ms);
+
 /* ---- GEMM + All-Scatter (Section 4, case study) --------------------------- */
 
 /* Bytes of the split-K workspace (symtile_gas_config.workspace) of a call

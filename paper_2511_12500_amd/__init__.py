@@ -16,7 +16,7 @@ _BINDING = (
     "symtile_gas_workspace_bytes", "symtile_gemm_all_scatter",
     "symtile_gemm_all_scatter_noalloc", "NOALLOC_SCRATCH_BYTES", "symtile_heap_alloc", "symtile_heap_bases", "symtile_litmus_mp", "symtile_heap_create", "symtile_heap_create_on",
     "symtile_heap_destroy", "symtile_heap_fill", "symtile_heap_info", "symtile_heap_ptr",
-    "symtile_last_error", "symtile_tile_copy", "symtile_translate", "symtile_translate_device",
+    "symtile_last_error", "symtile_tile_copy", "symtile_tile_copy_timed", "symtile_translate", "symtile_translate_device",
     "symtile_value_exercise", "symtile_version",
 )
 _HEAP = ("GatheredOutput", "Heap", "current_stream")

@@ -78,6 +78,8 @@ def _load():
         "symtile_atomic_exercise": [vp, i32, i32, i32, sz, i32, i32, i32, u32, u32, vp, vp],
         "symtile_tile_copy": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, i32, i32,
                               vp],
+        "symtile_tile_copy_timed": [vp, sz, sz, i32, i32, i32, i32, i32, i32, i32, i32, sz, i32,
+                                    i32, vp, ctypes.POINTER(ctypes.c_float)],
         "symtile_gemm_all_scatter": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
                                      i32, ctypes.POINTER(GasConfig), vp],
         "symtile_gemm_all_scatter_noalloc": [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32,
@@ -217,6 +219,19 @@ def symtile_tile_copy(h: int, src_off: int, dst_off: int, rows: int, cols: int, 
     _check(lib.symtile_tile_copy(_vp(h), src_off, dst_off, rows, cols, ld, dtype, tile_r, tile_c,
                                  shift, only_rank, flag_off, tiles_per_wg, mode, _vp(stream)),
            "symtile_tile_copy")
+
+
+def symtile_tile_copy_timed(h: int, src_off: int, dst_off: int, rows: int, cols: int, ld: int,
+                            dtype: int, tile_r: int, tile_c: int, shift: int, only_rank: int,
+                            flag_off: int, tiles_per_wg: int = 0, stream: int = 0,
+                            mode: int = 0) -> float:
+    """symtile_tile_copy with the kernel bracketed by events; waits for it and
+    returns its duration in ms."""
+    ms = ctypes.c_float()
+    _check(lib.symtile_tile_copy_timed(_vp(h), src_off, dst_off, rows, cols, ld, dtype, tile_r,
+                                       tile_c, shift, only_rank, flag_off, tiles_per_wg, mode,
+                                       _vp(stream), ctypes.byref(ms)), "symtile_tile_copy_timed")
+    return ms.value
 
 
 def symtile_gemm_all_scatter(h: int, A: int, B_shard: int, C_gathered_local: int,

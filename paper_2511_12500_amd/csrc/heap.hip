@@ -460,6 +460,8 @@ symtile_status symtile_heap_destroy(symtile_heap* h) {
     if (h->control) (void)hipFree(h->control);
     if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
     if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+    if (h->ev_t0) (void)hipEventDestroy(h->ev_t0);
+    if (h->ev_t1) (void)hipEventDestroy(h->ev_t1);
     if (h->aux_stream) (void)hipStreamDestroy(h->aux_stream);
     delete h;
     return st;

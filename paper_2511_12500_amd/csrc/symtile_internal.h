@@ -27,6 +27,9 @@ struct symtile_heap {
     // the heap.
     hipStream_t aux_stream;
     hipEvent_t ev_fork, ev_join;
+    // Events bracketing one kernel of a timed call (symtile_tile_copy_timed),
+    // created on first use and destroyed with the heap.
+    hipEvent_t ev_t0, ev_t1;
 };
 
 namespace symtile_host {

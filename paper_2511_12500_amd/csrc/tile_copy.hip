@@ -166,11 +166,15 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
 
 }  // namespace
 
-extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off,
-                                            int rows, int cols, int ld, int dtype, int tile_r,
-                                            int tile_c, int shift, int only_rank,
-                                            size_t flag_off, int tiles_per_wg, int mode,
-                                            symtile_stream s) {
+// The checks and launch of symtile_tile_copy; with t0 and t1 set the kernel
+// is launched with hipExtLaunchKernel, which records the two events as part
+// of the kernel's dispatch.
+static symtile_status tile_copy_launch(symtile_heap* h, size_t src_off, size_t dst_off, int rows,
+                                       int cols, int ld, int dtype, int tile_r, int tile_c,
+                                       int shift, int only_rank, size_t flag_off,
+                                       int tiles_per_wg, int mode, symtile_stream s,
+                                       hipEvent_t t0, hipEvent_t t1) {
+
     using symtile_host::fail;
     if (!h) return fail(SYMTILE_EINVAL, "heap is NULL");
     int esize = 0;
@@ -263,14 +267,57 @@ extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, siz
     if (symtile_status st = symtile_host::set_device(h, &prev)) return st;
     const dim3 grid((unsigned)((nitems + p.per_wg - 1) / p.per_wg));
     hipStream_t stream = static_cast<hipStream_t>(s);
+    const void* kernel;
     switch (p.tile_chunks) {
-        case 16: hipLaunchKernelGGL((tile_copy_kernel<16, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
-        case 32: hipLaunchKernelGGL((tile_copy_kernel<32, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
-        case 64: hipLaunchKernelGGL((tile_copy_kernel<64, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
-        default: hipLaunchKernelGGL((tile_copy_kernel<0, symtile::kStoreWriteThrough>), grid, dim3(kThreads), 0, stream, p); break;
+        case 16: kernel = reinterpret_cast<const void*>(&tile_copy_kernel<16, symtile::kStoreWriteThrough>); break;
+        case 32: kernel = reinterpret_cast<const void*>(&tile_copy_kernel<32, symtile::kStoreWriteThrough>); break;
+        case 64: kernel = reinterpret_cast<const void*>(&tile_copy_kernel<64, symtile::kStoreWriteThrough>); break;
+        default: kernel = reinterpret_cast<const void*>(&tile_copy_kernel<0, symtile::kStoreWriteThrough>); break;
     }
-    hipError_t e = hipGetLastError();
+    void* args[] = {&p};
+    hipError_t e = t0 ? hipExtLaunchKernel(kernel, grid, dim3(kThreads), args, 0, stream, t0, t1, 0)
+                      : hipLaunchKernel(kernel, grid, dim3(kThreads), args, 0, stream);
+    if (e == hipSuccess) e = hipGetLastError();
     (void)hipSetDevice(prev);
     if (e != hipSuccess) return symtile_host::hip_fail(e, "tile_copy_kernel launch");
+    return SYMTILE_OK;
+}
+
+extern "C" symtile_status symtile_tile_copy(symtile_heap* h, size_t src_off, size_t dst_off,
+                                            int rows, int cols, int ld, int dtype, int tile_r,
+                                            int tile_c, int shift, int only_rank,
+                                            size_t flag_off, int tiles_per_wg, int mode,
+                                            symtile_stream s) {
+    return tile_copy_launch(h, src_off, dst_off, rows, cols, ld, dtype, tile_r, tile_c, shift,
+                            only_rank, flag_off, tiles_per_wg, mode, s, nullptr, nullptr);
+}
+
+extern "C" symtile_status symtile_tile_copy_timed(symtile_heap* h, size_t src_off,
+                                                  size_t dst_off, int rows, int cols, int ld,
+                                                  int dtype, int tile_r, int tile_c, int shift,
+                                                  int only_rank, size_t flag_off,
+                                                  int tiles_per_wg, int mode, symtile_stream s,
+                                                  float* kernel_ms) {
+    using symtile_host::fail;
+    if (!h) return fail(SYMTILE_EINVAL, "heap is NULL");
+    if (!kernel_ms) return fail(SYMTILE_EINVAL, "kernel_ms is NULL");
+    *kernel_ms = 0.0f;
+    int prev = -1;
+    if (symtile_status st = symtile_host::set_device(h, &prev)) return st;
+    struct Restore {
+        int d;
+        ~Restore() {
+            if (d >= 0) (void)hipSetDevice(d);
+        }
+    } restore{prev};
+    if (!h->ev_t0) SYMTILE_HIP(hipEventCreate(&h->ev_t0));
+    if (!h->ev_t1) SYMTILE_HIP(hipEventCreate(&h->ev_t1));
+    if (symtile_status st = tile_copy_launch(h, src_off, dst_off, rows, cols, ld, dtype, tile_r,
+                                             tile_c, shift, only_rank, flag_off, tiles_per_wg,
+                                             mode, s, h->ev_t0, h->ev_t1))
+        return st;
+    if (rows == 0 || cols == 0) return SYMTILE_OK;   // nothing launched
+    SYMTILE_HIP(hipEventSynchronize(h->ev_t1));
+    SYMTILE_HIP(hipEventElapsedTime(kernel_ms, h->ev_t0, h->ev_t1));
     return SYMTILE_OK;
 }

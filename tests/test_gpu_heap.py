@@ -277,6 +277,36 @@ def test_heap_tile_copy_workload_bitexact(tile, per_wg, mode):
     assert np.array_equal(fl, want_flags.astype(np.int32))
 
 
+@pytest.mark.parametrize("tile", [64, 128, 256])
+def test_heap_tile_copy_timed_matches_untimed(tile):
+    """symtile_tile_copy_timed leaves the same heap as symtile_tile_copy (the
+    oracle's ring copy, every counter at 1 after one call, at 2 after the
+    second) and reports a positive kernel duration; an empty copy reports 0."""
+    pkg = sym()
+    wl = workload.HEAP_COPY
+    heap, src, dst, flags = _copy_heap(pkg, wl.world, wl.rows, wl.cols, torch.float32)
+    send = workload.copy_send(wl, seed=3)
+    heap.slots_view(src, (wl.rows, wl.cols), torch.float32).copy_(send.cuda())
+    heap.slots_view(dst, (wl.rows, wl.cols), torch.int32).fill_(-1)
+    ms = pkg.symtile_tile_copy_timed(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, pkg.F32,
+                                     tile, tile, wl.shift, -1, flags,
+                                     stream=pkg.current_stream())
+    assert 0.0 < ms < 100.0
+    pkg.symtile_tile_copy(heap.handle, src, dst, wl.rows, wl.cols, wl.cols, pkg.F32, tile, tile,
+                          wl.shift, -1, flags, stream=pkg.current_stream())
+    heap.barrier()
+    recv = heap.slots_view(dst, (wl.rows, wl.cols), torch.float32).cpu().numpy()
+    ntiles = (wl.rows // tile) * (wl.cols // tile)
+    fl = heap.slots_view(flags, (ntiles,), torch.int32).cpu().numpy()
+    want, want_flags = oracle.tile_copy(send.numpy(), np.full_like(send.numpy(), np.nan),
+                                        tile, tile, wl.shift)
+    assert np.array_equal(recv.view(np.uint32), want.view(np.uint32))
+    assert np.array_equal(fl, 2 * want_flags.astype(np.int32))
+    assert pkg.symtile_tile_copy_timed(heap.handle, src, dst, 0, wl.cols, wl.cols, pkg.F32,
+                                       tile, tile, 1, -1, flags) == 0.0
+    heap.barrier()
+
+
 @pytest.mark.parametrize("mode", [0, 1], ids=["put", "get"])
 @pytest.mark.parametrize("case", [(5, 100, 72, 32, 24, 3, "bf16"), (3, 33, 20, 16, 8, 1, "f32"),
                                   (8, 64, 64, 64, 64, 7, "f16")])
