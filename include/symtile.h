@@ -121,7 +121,26 @@ typedef struct {
                              workspace must not overlap in time (same stream, or
                              synchronised). */
     size_t workspace_bytes;
+    int split_reduce;     /* split_k > 1: who sums a tile's K slices (symtile_split_reduce).
+                             SYMTILE_SPLIT_REDUCE_LAST: the slice that arrives last
+                             sums all partials and stores the whole tile (any grid).
+                             SYMTILE_SPLIT_REDUCE_BANDED: the tile's rows form
+                             split_k bands and slice s sums and stores band s, so
+                             the reduction and the stores are spread over all
+                             slices; needs one co-resident workgroup per slice
+                             (tiles * split_k <= symtile_device_info's
+                             max_coresident_wgs, gemm_wgs 0 or tiles * split_k) and
+                             tile_m / split_k a multiple of 32 (16 for 256x224),
+                             else EUNSUPPORTED.  0 = BANDED where it applies and
+                             split_k = 2, else LAST.  Both give the same bits. */
 } symtile_gas_config;
+
+/* Reduction of split-K slices (symtile_gas_config.split_reduce). */
+typedef enum {
+    SYMTILE_SPLIT_REDUCE_AUTO = 0,
+    SYMTILE_SPLIT_REDUCE_LAST = 1,
+    SYMTILE_SPLIT_REDUCE_BANDED = 2
+} symtile_split_reduce;
 
 /* Per-tile trace record.  Times are ticks of the device's constant-rate
  * realtime counter (symtile_clock_rate_khz), comparable across workgroups.
@@ -253,8 +272,19 @@ typedef enum {
     SYMTILE_MP_RELAXED = 0,  /* relaxed +1, relaxed polls, no fences (no guarantee) */
     SYMTILE_MP_FENCES = 1,   /* release fence + relaxed +1; relaxed polls + acquire fence */
     SYMTILE_MP_RMW = 2,      /* fetch_add(+1, release); polls by fetch_add(0, acquire) */
-    SYMTILE_MP_CAS = 3       /* cas(i-1 -> i, release); polls by cas(i -> i, acquire), the lock
+    SYMTILE_MP_CAS = 3,      /* cas(i-1 -> i, release); polls by cas(i -> i, acquire), the lock
                                 handshake of the workgroup-specialised listing (Section 4.2.2) */
+    SYMTILE_MP_WT = 4,       /* data stored write-through (the stores' cache-policy bits
+                                sc0 sc1), released by waiting for their acknowledgement
+                                only (no L2 write-back), relaxed +1; relaxed polls +
+                                acquire fence (the kernels' write-through publication) */
+    SYMTILE_MP_ACK = 5,      /* the same release with ordinary write-back data stores:
+                                the control, which the write-back fence exists for */
+    SYMTILE_MP_WT_COHERENT = 6, /* SYMTILE_MP_WT's writer; the reader polls, then reads
+                                the data with coherent loads (sc0 sc1) and no acquire
+                                fence (no L2 invalidate) */
+    SYMTILE_MP_WT_PLAIN = 7  /* SYMTILE_MP_WT's writer; the reader polls and reads with
+                                ordinary loads, no acquire fence: the control */
 } symtile_mp_form;
 
 /* Message-passing litmus test of the flag protocol (Section 3.3.3, memory

@@ -106,6 +106,18 @@ __device__ __forceinline__ u32x4 buf_ld16(rsrc_t r, uint32_t voff, uint32_t soff
 //                      where the destination is not read again soon).
 enum : int { kStoreDefault = 0, kStoreNonTemporal = 2, kStoreWriteThrough = 17 };
 
+// Load cache policies: kLoadDefault may hit a line this XCD's L2 holds from
+// before; kLoadCoherent (sc0 sc1, the encoding the memory model gives a
+// system-scope relaxed atomic load) reads the value that is coherent for
+// every XCD, not a copy the L2 kept.
+enum : int { kLoadDefault = 0, kLoadCoherent = 17 };
+
+template <int POLICY>
+__device__ __forceinline__ u32x4 buf_ld16p(rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, voff, __builtin_amdgcn_readfirstlane(soff),
+                                                 POLICY);
+}
+
 template <int POLICY>
 __device__ __forceinline__ void buf_st16p(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
     __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, __builtin_amdgcn_readfirstlane(soff),
@@ -247,6 +259,26 @@ __device__ __forceinline__ void wg_stores_done() {
     __syncthreads();
 }
 
+// Release of write-through stores.  An agent- or system-scope release fence
+// writes back the XCD's L2 (buffer_wbl2), because ordinary stores may sit
+// dirty in it; that write-back costs about as much whether or not anything
+// is dirty, and the write-backs of one XCD's workgroups run one after
+// another.  Stores issued with kStoreWriteThrough carry the system-coherence
+// bits (sc0 sc1), the same encoding the memory model gives a system-scope
+// relaxed atomic store: they leave no dirty line, and their acknowledgement
+// (vmcnt) comes back once they are coherent for every XCD.  For data written
+// only that way, waiting for the acknowledgements is the whole release: the
+// caller has already waited for them (wg_stores_done), and this adds the
+// compiler barrier that keeps the counter update after the stores.  The
+// reader still acquires (flag_wait), which invalidates its own L2's copies.
+// Covers only stores this workgroup made with kStoreWriteThrough; any other
+// store that the reader must see needs fence_release.  The message-passing
+// litmus test exercises exactly this form (symtile_litmus_mp, SYMTILE_MP_WT).
+__device__ __forceinline__ void release_written_through() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    asm volatile("" ::: "memory");
+}
+
 template <int SCOPE = __HIP_MEMORY_SCOPE_AGENT>
 __device__ __forceinline__ void flag_signal(uint32_t* flag) {
     __hip_atomic_fetch_add(global_ptr(flag), 1u, __ATOMIC_RELAXED, SCOPE);
@@ -255,6 +287,30 @@ __device__ __forceinline__ void flag_signal(uint32_t* flag) {
 template <int SCOPE = __HIP_MEMORY_SCOPE_AGENT>
 __device__ __forceinline__ void flag_publish(uint32_t* flag) {
     fence_release<SCOPE>();
+    flag_signal<SCOPE>(flag);
+}
+
+// Acquire for data read with kLoadCoherent only, the mirror of
+// release_written_through: an agent- or system-scope acquire fence
+// invalidates the XCD's L2 (and the CU's L1) so that later ordinary loads
+// miss copies of lines that another XCD has since rewritten; like the
+// write-back, the invalidate costs about the same whatever the L2 holds, and
+// one XCD's run one after another.  Loads issued with kLoadCoherent do not
+// take such copies, so after a poll that saw the counter the acquire needs
+// only the order of the accesses: the poll's value is waited for (its
+// result decides the branch) and the compiler barrier keeps the data loads
+// after it.  Covers only loads made with kLoadCoherent; other loads of the
+// published data need fence_acquire.  Litmus: SYMTILE_MP_WT_COHERENT.
+__device__ __forceinline__ void acquire_coherent_reads() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the poll has returned
+    asm volatile("" ::: "memory");
+}
+
+// flag_publish for data written with kStoreWriteThrough only (see
+// release_written_through).
+template <int SCOPE = __HIP_MEMORY_SCOPE_AGENT>
+__device__ __forceinline__ void flag_publish_written_through(uint32_t* flag) {
+    release_written_through();
     flag_signal<SCOPE>(flag);
 }
 
@@ -281,6 +337,16 @@ __device__ __forceinline__ bool flag_wait(const uint32_t* flag, uint32_t target,
                                           uint32_t spin_limit) {
     if (!flag_poll<SCOPE>(flag, target, spin_limit)) return false;
     fence_acquire<SCOPE>();
+    return true;
+}
+
+// flag_wait for data read with kLoadCoherent only: flag_poll, then on
+// success acquire_coherent_reads instead of the L2-invalidating fence.
+template <int SCOPE = __HIP_MEMORY_SCOPE_AGENT>
+__device__ __forceinline__ bool flag_wait_coherent(const uint32_t* flag, uint32_t target,
+                                                   uint32_t spin_limit) {
+    if (!flag_poll<SCOPE>(flag, target, spin_limit)) return false;
+    acquire_coherent_reads();
     return true;
 }
 
@@ -402,8 +468,8 @@ __device__ __forceinline__ void get(const void* src, void* dst, const TileGeom& 
 // once, is written to the same place in the heaps of ranks (cur + d) mod
 // world for d in [d0, d1) -- the consumer copy of the producer/consumer
 // schedules, which sends a finished tile to every other rank.  U passes are
-// loaded, then stored to each rank in turn.
-template <int POLICY, int U>
+// loaded (with load policy LOAD), then stored to each rank in turn.
+template <int POLICY, int U, int LOAD = kLoadDefault>
 __device__ __forceinline__ void put_ranks(const void* p, const TileGeom& g, int cur, int d0,
                                           int d1, int world, const uint64_t* __restrict__ bases,
                                           int tid, int threads) {
@@ -413,7 +479,8 @@ __device__ __forceinline__ void put_ranks(const void* p, const TileGeom& g, int 
     for (int b = 0; b < L.passes; b += U) {
         u32x4 v[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = buf_ld16(rs, L.voff, (uint32_t)(b + u) * L.pass_bytes);
+        for (int u = 0; u < U; ++u)
+            v[u] = buf_ld16p<LOAD>(rs, L.voff, (uint32_t)(b + u) * L.pass_bytes);
         for (int d = d0; d < d1; ++d) {
             const rsrc_t rd = tile_rsrc(p, g, cur, (cur + d) % world, bases);
 #pragma unroll

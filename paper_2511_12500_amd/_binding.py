@@ -9,12 +9,14 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsymtile.
 
 F16, BF16, F32 = 1, 2, 3
 BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC, WAVE_SPEC = 0, 1, 2, 3, 4
+SPLIT_REDUCE_AUTO, SPLIT_REDUCE_LAST, SPLIT_REDUCE_BANDED = 0, 1, 2
 PUT, GET = 0, 1
 LOAD, STORE = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}
 SEMS = {"relaxed": 0, "acquire": 1, "release": 2, "acq_rel": 3}
 SCOPES = {"block": 0, "gpu": 1, "sys": 2}
-MP_FORMS = {"relaxed": 0, "fences": 1, "rmw": 2, "cas": 3}
+MP_FORMS = {"relaxed": 0, "fences": 1, "rmw": 2, "cas": 3, "wt": 4, "ack": 5,
+            "wt_coherent": 6, "wt_plain": 7}
 SB_FORMS = {"relaxed": 0, "acq_rel": 1, "seq_cst": 2}
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "ENOMEM", -3: "EHIP", -4: "ETIMEOUT", -5: "EUNSUPPORTED"}
@@ -48,6 +50,7 @@ class GasConfig(ctypes.Structure):
         ("split_k", ctypes.c_int),
         ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t),
+        ("split_reduce", ctypes.c_int),
     ]
 
 

@@ -90,6 +90,10 @@ struct GasParams {
     int split, units;
     uint32_t* sk_cnt;       // [num_tiles][2]: arrival ticket, partials written
     float* sk_part;         // [num_tiles][split][BM*BN] fp32 partial tiles
+    // Banded reduction (every unit has its own co-resident workgroup): slice
+    // s sums and stores tile rows [s*BM/split, (s+1)*BM/split); 0 = the last
+    // slice to arrive sums and stores the whole tile.
+    int sk_band;
 };
 
 // Trace record of tile (tm, tn), or nullptr when tracing is off.
@@ -265,6 +269,24 @@ __device__ __forceinline__ void with_store_policy(int mode, F&& f) {
         f(std::integral_constant<int, symtile::kStoreDefault>{});
 }
 
+// Release of this workgroup's output stores before their counters move
+// (agent scope): stores written through need only their acknowledgement,
+// the other policies the L2 write-back of a release fence.
+template <int POLICY>
+__device__ __forceinline__ void release_output() {
+    if constexpr (POLICY == symtile::kStoreWriteThrough)
+        symtile::release_written_through();
+    else
+        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
+}
+
+__device__ __forceinline__ void release_output(int mode) {
+    if (mode == 2)
+        symtile::release_written_through();
+    else
+        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
+}
+
 // Geometry of output tile (tm, tn) for the tile verbs: 16-bit elements, so
 // 8 per 16-byte chunk; THREADS threads cover CPR chunk columns per pass.
 template <int BM, int BN, int THREADS>
@@ -284,16 +306,18 @@ __device__ __forceinline__ uint16_t* out_tile_ptr(const GasParams& p, int BM, in
 }
 
 // Copy one finished tile from the local heap to every other heap (the put of
-// Sections 4.1.1 and 4.2.2) and release its counters there.
-template <int BM, int BN, int THREADS, int POLICY>
+// Sections 4.1.1 and 4.2.2) and release its counters there.  LOAD is the
+// policy of the tile's loads (coherent after a flag_wait_coherent).
+template <int BM, int BN, int THREADS, int POLICY, int LOAD = symtile::kLoadDefault>
 __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
     using IO = TileIO<BM, BN, THREADS>;
     const int tid = threadIdx.x;
-    symtile::put_ranks<POLICY, IO::U>(out_tile_ptr(p, BM, BN, tm, tn), out_tile<BM, BN, THREADS>(p, tm, tn),
-                                      p.rank, 1, p.world, p.world, p.bases, tid, THREADS);
+    symtile::put_ranks<POLICY, IO::U, LOAD>(out_tile_ptr(p, BM, BN, tm, tn),
+                                            out_tile<BM, BN, THREADS>(p, tm, tn), p.rank, 1,
+                                            p.world, p.world, p.bases, tid, THREADS);
     symtile::wg_stores_done();
     if (tid < 64) {            // wave 0: one release, then lane d counts slot rank + d
-        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
+        release_output<POLICY>();
         uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
         const int d = tid + 1;
         if (d < p.world)
@@ -305,7 +329,9 @@ __device__ void put_tile_to_peers(const GasParams& p, int tm, int tn) {
 // 4.2.2): consumer `cid` of `ncons` takes tiles cid, cid + ncons, ... in the
 // producers' tile order, waits (bounded) until the producer's ready counter
 // reaches the epoch, acquires, and puts the tile to the other heaps.  A
-// timed-out wait records ERR_TIMEOUT and ends this consumer.
+// timed-out wait records ERR_TIMEOUT and ends this consumer.  With the
+// write-through output policy the producers' tiles are read back with
+// coherent loads, so the acquire needs no L2 invalidate.
 template <int BM, int BN, int THREADS>
 __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
     __shared__ int s_ok;
@@ -316,8 +342,10 @@ __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
         uint64_t* tr = tile_trace(p, tm, tn);
         if (tid == 0) {
             if (tr) tr[SYMTILE_TRACE_COPY_WAIT] = symtile::clock_now();
-            const bool ok =
-                symtile::flag_wait(p.ready + tm * p.tiles_n + tn, p.epoch, p.spin_limit);
+            const uint32_t* rdy = p.ready + tm * p.tiles_n + tn;
+            const bool ok = p.nontemporal == 2
+                                ? symtile::flag_wait_coherent(rdy, p.epoch, p.spin_limit)
+                                : symtile::flag_wait(rdy, p.epoch, p.spin_limit);
             if (!ok) symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
             if (tr) tr[SYMTILE_TRACE_COPY_GO] = symtile::clock_now();
             s_ok = ok;
@@ -325,7 +353,10 @@ __device__ void consume_tiles(const GasParams& p, int cid, int ncons) {
         __syncthreads();
         if (!s_ok) return;
         with_store_policy(p.nontemporal, [&](auto pol) {
-            put_tile_to_peers<BM, BN, THREADS, decltype(pol)::value>(p, tm, tn);
+            constexpr int P = decltype(pol)::value;
+            put_tile_to_peers<BM, BN, THREADS, P,
+                              P == symtile::kStoreWriteThrough ? symtile::kLoadCoherent
+                                                               : symtile::kLoadDefault>(p, tm, tn);
         });
         if (tr && tid == 0) tr[SYMTILE_TRACE_COPY_DONE] = symtile::clock_now();
     }
@@ -391,7 +422,7 @@ __device__ void copy_wave_tiles(const GasParams& p, int KT) {
         };
         auto publish = [&]() {
             __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();  // one release; lane d counts slot rank + d
+            release_output<POLICY>();                 // one release; lane d counts slot rank + d
             uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + ptm) * p.tiles_n + ptn;
             if (lane >= 1 && lane < p.world)
                 symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + lane) % p.world,
@@ -752,16 +783,30 @@ void gas_kernel(const GasParams p) {
             tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
 
         // ---- split-K: combine the K slices of the tile ------------------
-        // Every slice takes an arrival ticket.  A slice that is not the last
-        // to arrive writes its fp32 partial tile, releases it and counts it
-        // as written, and moves on.  The last one waits until the others'
-        // partials are written: they all took their tickets before it, so
-        // they are running and wait for nothing themselves (no deadlock, and
-        // no co-residency is assumed).  It then acquires them and forms the
-        // sum in slice order, so the result does not depend on which slice
-        // came last, and goes on to the epilogue with the tile's full sum.
-        // (not built into the copy-wave kernel: wave specialisation has no
-        // split-K, and its third wave per SIMD leaves no registers for it)
+        // Every slice takes an arrival ticket (counter 0 of the tile).
+        //  * Last-arriver protocol (p.sk_band == 0): a slice that is not the
+        //    last to arrive writes its fp32 partial tile, releases it and
+        //    counts it as written (counter 1), and moves on.  The last one
+        //    waits until the others' partials are written: they all took
+        //    their tickets before it, so they are running and wait for
+        //    nothing themselves (no deadlock, and no co-residency is
+        //    assumed).  It acquires them, forms the sum in slice order, and
+        //    runs the epilogue for the whole tile.
+        //  * Banded protocol (p.sk_band == 1, chosen by the host only when
+        //    every work unit has a workgroup of its own and all of them are
+        //    resident at once): the tile's rows form split bands; slice s
+        //    writes its partial for the rows of the other bands, counts
+        //    itself, waits until every slice has, and then sums band s in
+        //    slice order and stores band s.  The reduction and the stores are
+        //    shared by all slices instead of falling on the last one.
+        // Either way the sum is p0 + p1 + ... in slice order, so both give
+        // the same bits, whichever slice came last.  (Not built into the
+        // copy-wave kernel: wave specialisation has no split-K, and its
+        // third wave per SIMD leaves no registers for it.)
+        const bool banded = !CW && p.split > 1 && p.sk_band != 0;
+        const int band_rows = banded ? BM / p.split : BM;
+        // band of accumulator block row i of this wave (blocks are MF rows)
+        auto block_band = [&](int i) { return (wm * WM + i * MF) / band_rows; };
         if (!CW && p.split > 1) {
             __shared__ uint32_t s_ticket, s_ok;
             const int tile = tm * p.tiles_n + tn;
@@ -777,17 +822,29 @@ void gas_kernel(const GasParams p) {
                 if (tid == 0) symtile::raise_error(p.err, symtile::ERR_WORKSPACE);
                 continue;
             }
-            const bool last = ticket + 1 == (uint32_t)p.split;
+            const bool last = !banded && ticket + 1 == (uint32_t)p.split;
             // Partial tile of slice q: each thread's accumulators, 16 bytes
             // per (i, j, 4-value group), so a wave's access is 1 KiB contiguous.
             auto slot = [&](int q) {
                 return symtile::make_rsrc(p.sk_part + ((size_t)tile * p.split + q) * (BM * BN),
                                           (uint32_t)(BM * BN * 4));
             };
+            // Blocks of this thread's accumulators that a step covers: all of
+            // them, or (banded) the ones in this slice's band (`own`) or
+            // outside it.
+            auto covered = [&](int i, bool own) {
+                return !banded || ((block_band(i) == ks) == own);
+            };
+            // With large accumulators and more than two slices the reducing
+            // slice sums every partial from memory, its own included, so
+            // its own rows go to memory too.
+            constexpr bool kBig = MI * NI * ACC_N > 64;
+            const bool own_to_memory = kBig && p.split > 2;
             auto put_partial = [&](int q) {
                 const symtile::rsrc_t rs = slot(q);
 #pragma unroll
-                for (int i = 0; i < MI; ++i)
+                for (int i = 0; i < MI; ++i) {
+                    if (!own_to_memory && !covered(i, false)) continue;
 #pragma unroll
                     for (int j = 0; j < NI; ++j)
 #pragma unroll
@@ -801,11 +858,13 @@ void gas_kernel(const GasParams p) {
                                 v, rs, (uint32_t)tid * 16,
                                 (uint32_t)(((i * NI + j) * (ACC_N / 4) + g) * THREADS * 16));
                         }
+                }
             };
             // dst = partial q (first) or dst + partial q, in batches of 8
             // loads (32 registers): scheduling fences keep the compiler from
             // hoisting every load at once, which would need 4 registers per
-            // accumulator register.
+            // accumulator register.  Blocks outside the covered set are not
+            // touched.
             auto add_partial = [&](acc_t (&dst)[MI][NI], int q, bool first) {
                 const symtile::rsrc_t rs = slot(q);
                 constexpr int GPA = ACC_N / 4;                 // 4-value groups per accumulator
@@ -816,12 +875,16 @@ void gas_kernel(const GasParams p) {
                 for (int b = 0; b < NG; b += BATCH) {
                     symtile::u32x4 v[BATCH];
 #pragma unroll
-                    for (int x = 0; x < BATCH; ++x)
-                        v[x] = symtile::buf_ld16(rs, (uint32_t)tid * 16,
-                                                 (uint32_t)((b + x) * THREADS * 16));
+                    for (int x = 0; x < BATCH; ++x) {
+                        const int i = (b + x) / (NI * GPA);
+                        v[x] = symtile::buf_ld16p<symtile::kLoadCoherent>(
+                            rs, covered(i, true) ? (uint32_t)tid * 16 : symtile::kOOB,
+                            (uint32_t)((b + x) * THREADS * 16));
+                    }
 #pragma unroll
                     for (int x = 0; x < BATCH; ++x) {
                         const int n = b + x, i = n / (NI * GPA), j = (n / GPA) % NI, g = n % GPA;
+                        if (!covered(i, true)) continue;
                         const f32x4_t y = __builtin_bit_cast(f32x4_t, v[x]);   // whole vector
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
@@ -830,20 +893,31 @@ void gas_kernel(const GasParams p) {
                     __builtin_amdgcn_sched_barrier(0);
                 }
             };
+            // 1. partials: every slice but the last-arriving one (banded:
+            // every slice, for the other bands' rows), and the reducing
+            // slice's own rows when it sums from memory
+            if (!last || own_to_memory) put_partial(ks);
             if (!last) {
-                put_partial(ks);
                 symtile::wg_stores_done();
-                if (tid == 0) symtile::flag_publish(cnt + 1);
-                continue;
+                // (partials are always stored write-through)
+                if (tid == 0) symtile::flag_publish_written_through(cnt + 1);
+                if (!banded) continue;
+            } else if (own_to_memory) {
+                __builtin_amdgcn_s_waitcnt(vm_wait(0));
             }
+            // 2. wait for the others' partials (bounded); they were written
+            // through and are read with coherent loads, so the wait needs
+            // no L2 invalidate
             if (tid == 0) {
-                const bool ok = symtile::flag_wait(cnt + 1, (uint32_t)p.split - 1, p.spin_limit);
-                if (ok) {
+                const uint32_t target = banded ? (uint32_t)p.split : (uint32_t)p.split - 1;
+                const bool ok = symtile::flag_wait_coherent(cnt + 1, target, p.spin_limit);
+                if (ok && !banded) {
                     // every slice of this call has counted itself: the next
-                    // call starts again from zero
+                    // call starts again from zero (banded: reset by the last
+                    // slice to store its band, below)
                     symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
                     symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
-                } else {
+                } else if (!ok) {
                     // a slice that holds a ticket may still count itself
                     // later, so the counters are left as they are: the next
                     // call that uses this workspace then draws tickets past
@@ -855,7 +929,8 @@ void gas_kernel(const GasParams p) {
             }
             __syncthreads();
             if (!s_ok) continue;
-            if constexpr (MI * NI * ACC_N <= 64) {
+            // 3. the sum in slice order over the covered blocks
+            if constexpr (!kBig) {
                 // Small accumulators fold in registers:
                 // tmp = p0 + ... + p(ks-1), acc = tmp + acc, which is
                 // (p0 + ... + p(ks-1)) + p(ks) since addition commutes, then
@@ -868,19 +943,17 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                         for (int j = 0; j < NI; ++j)
 #pragma unroll
-                            for (int e = 0; e < ACC_N; ++e) acc[i][j][e] = tmp[i][j][e] + acc[i][j][e];
+                            for (int e = 0; e < ACC_N; ++e)
+                                if (covered(i, true)) acc[i][j][e] = tmp[i][j][e] + acc[i][j][e];
                 }
                 for (int q = ks + 1; q < p.split; ++q) add_partial(acc, q, false);
             } else {
                 // Two slices: acc + the other partial, which is p0 + p1 either
                 // way (fp32 addition commutes).  More: this slice's partial
-                // joins the others in memory and the sum is formed
-                // p0 + p1 + ... in slice order.  (One call site of add_partial:
-                // with two, the compiler spills inside the K loop.)
-                if (p.split > 2) {
-                    put_partial(ks);
-                    __builtin_amdgcn_s_waitcnt(vm_wait(0));
-                }
+                // joined the others in memory and the sum is formed
+                // p0 + p1 + ... in slice order.  (One call site of
+                // add_partial: with two, the compiler spills inside the K
+                // loop.)
                 const int nq = p.split == 2 ? 1 : p.split;
                 for (int n = 0; n < nq; ++n)
                     add_partial(acc, p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
@@ -888,9 +961,11 @@ void gas_kernel(const GasParams p) {
         }
 
         // ---- epilogue: round, restage row-major, store, release --------
+        // (banded split-K: only this slice's band is restaged and stored)
         uint8_t* Cs = smem;
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+        for (int i = 0; i < MI; ++i) {
+            if (banded && block_band(i) != ks) continue;
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
@@ -908,6 +983,7 @@ void gas_kernel(const GasParams p) {
                     *reinterpret_cast<uint2*>(Cs + row * CROW + ((chunk ^ (row & 7)) << 4) +
                                               (half << 3)) = w;
                 }
+        }
         __syncthreads();
 
         // FUSED: every slot.  WAVE_SPEC: the local slot (the copy wave does the
@@ -921,32 +997,67 @@ void gas_kernel(const GasParams p) {
         const uint32_t voff = lanes.voff;
         const uint32_t pass_bytes = lanes.pass_bytes;
         const uint8_t* crow = Cs + r0 * CROW + ((c ^ (r0 & 7)) << 4);
+        // passes [pass_lo, pass_hi) hold the rows to store: the whole tile,
+        // or this slice's band (the host checks that a band is a whole
+        // number of passes)
+        const int pass_lo = banded ? ks * (band_rows / IO::RP) : 0;
+        const int pass_hi = banded ? pass_lo + band_rows / IO::RP : IO::PASSES;
 #pragma unroll 1
-        for (int b = 0; b < IO::PASSES; b += IO::U) {
+        for (int b = pass_lo; b < pass_hi; b += IO::U) {
             symtile::u32x4 v[IO::U];
 #pragma unroll
             for (int u = 0; u < IO::U; ++u)
-                v[u] = *reinterpret_cast<const symtile::u32x4*>(crow + (b + u) * IO::RP * CROW);
+                v[u] = *reinterpret_cast<const symtile::u32x4*>(
+                    crow + min(b + u, IO::PASSES - 1) * IO::RP * CROW);
             for (int d = 0; d < n_dst; ++d) {
                 const symtile::rsrc_t rd =
                     symtile::tile_rsrc(tile_local, geom, p.rank, (p.rank + d) % p.world, p.bases);
                 with_store_policy(p.nontemporal, [&](auto pol) {
 #pragma unroll
                     for (int u = 0; u < IO::U; ++u)
-                        symtile::buf_st16p<decltype(pol)::value>(v[u], rd, voff,
-                                                                 (b + u) * pass_bytes);
+                        if (b + u < pass_hi)       // uniform: a band may be one pass
+                            symtile::buf_st16p<decltype(pol)::value>(v[u], rd, voff,
+                                                                     (b + u) * pass_bytes);
                 });
             }
         }
         symtile::wg_stores_done();     // also orders the LDS reads above before reuse
         if (tid < 64) {                // wave 0: one release, then lane d counts slot rank + d
-            if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
-            symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
-            uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
-            if (tid < n_dst)
-                symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + tid) % p.world, p.bases));
-            if (tid == 0 && p.role == ROLE_WG_SPEC) symtile::flag_signal(p.ready + tm * p.tiles_n + tn);
-            if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
+            bool publish = true;
+            if (banded) {
+                // Banded: the tile is whole once every slice has stored its
+                // band.  Each slice releases its stores and takes a second
+                // ticket on counter 0 (the first round of tickets left it at
+                // split); the one that draws 2*split - 1 acquires the others'
+                // stores, resets the counters for the next call and publishes
+                // the tile's counters behind a release of its own.
+                release_output(p.nontemporal);
+                uint32_t* cnt = p.sk_cnt + 2 * (tm * p.tiles_n + tn);
+                uint32_t u2 = 0;
+                if (tid == 0)
+                    u2 = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
+                u2 = __shfl(u2, 0);
+                publish = u2 == 2u * (uint32_t)p.split - 1u;
+                if (publish) {
+                    // the other slices' band stores happen before the counters
+                    // move: written through, they were in memory before their
+                    // slices' tickets; otherwise acquire their releases
+                    if (p.nontemporal != 2) symtile::fence_acquire<__HIP_MEMORY_SCOPE_AGENT>();
+                    if (tid == 0) {
+                        symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
+                        symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                    }
+                }
+            }
+            if (publish) {
+                if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_STORED] = symtile::clock_now();
+                release_output(p.nontemporal);
+                uint32_t* flag = p.arrived + ((size_t)p.rank * p.tiles_m + tm) * p.tiles_n + tn;
+                if (tid < n_dst)
+                    symtile::flag_signal(symtile::translate(flag, p.rank, (p.rank + tid) % p.world, p.bases));
+                if (tid == 0 && p.role == ROLE_WG_SPEC) symtile::flag_signal(p.ready + tm * p.tiles_n + tn);
+                if (p.trace && tid == 0) tile_trace(p, tm, tn)[SYMTILE_TRACE_RELEASED] = symtile::clock_now();
+            }
         }
     }
 }
@@ -989,7 +1100,16 @@ struct Variant {
     const void* consumer;
     int copy_threads;            // workgroup size of scatter_kernel and consumer_kernel
     const void* gas_ws;          // wave-specialised kernel (NW compute waves + 1), or null
+    int band_q;                  // banded split-K: a band's rows must be a multiple of this
 };
+
+// Rows of a banded split-K reduction band must cover whole MFMA accumulator
+// blocks (MF rows) and whole passes of the epilogue's row stores.
+template <int BM, int BN, int NW, int MF>
+constexpr int band_quantum() {
+    constexpr int rp = TileIO<BM, BN, 64 * NW>::RP;
+    return rp > MF ? rp : MF;
+}
 
 // The copy-wave kernel is instantiated only for the shapes that use it.
 template <int BM, int BN, bool BF16, int NW, int MF, bool WS>
@@ -1006,7 +1126,8 @@ Variant make_variant() {
                    reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF>),
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>),
                    reinterpret_cast<const void*>(&consumer_kernel<BM, BN>),
-                   copy_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>()};
+                   copy_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>(),
+                   band_quantum<BM, BN, NW, MF>()};
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
@@ -1147,6 +1268,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     if (cfg.waves_per_wg != 0 && cfg.waves_per_wg != 4 && cfg.waves_per_wg != 8)
         return fail(SYMTILE_EINVAL, "waves_per_wg must be 0, 4 or 8");
     if (cfg.split_k < 0 || cfg.split_k > kMaxSplit) return fail(SYMTILE_EINVAL, "split_k must be 0..64");
+    if (cfg.split_reduce < SYMTILE_SPLIT_REDUCE_AUTO || cfg.split_reduce > SYMTILE_SPLIT_REDUCE_BANDED)
+        return fail(SYMTILE_EINVAL, "split_reduce must be 0, 1 or 2");
     const int split = cfg.split_k > 1 ? cfg.split_k : 1;
     if (split > 1 && cfg.variant != SYMTILE_FUSED_SEQ && cfg.variant != SYMTILE_BULK_SYNC)
         return fail(SYMTILE_EUNSUPPORTED, "split_k > 1 is built for BULK_SYNC and FUSED_SEQ");
@@ -1256,10 +1379,30 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     } restore{prev};
 
     const int ntiles = (int)num_tiles;
+    p.sk_band = 0;
     if (cfg.variant == SYMTILE_FUSED_SEQ || cfg.variant == SYMTILE_BULK_SYNC) {
         int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : std::min(p.units, cus);
         g = std::min(g, p.units);
         p.gemm_wgs = g;
+        if (split > 1) {
+            // Banded reduction: every slice waits for all the others, so
+            // every work unit needs a workgroup of its own, all resident at
+            // once; a band covers whole accumulator blocks and store passes.
+            const bool fits = g == p.units && g <= limit && cfg.tile_m % split == 0 &&
+                              (cfg.tile_m / split) % v->band_q == 0;
+            if (cfg.split_reduce == SYMTILE_SPLIT_REDUCE_BANDED && !fits)
+                return fail(SYMTILE_EUNSUPPORTED,
+                            "banded split-K reduction needs one resident workgroup per K slice "
+                            "(tiles * split_k <= " + std::to_string(limit) +
+                                ") and tile_m / split_k a multiple of " +
+                                std::to_string(v->band_q));
+            // AUTO: banded for two slices, where each slice reduces half the
+            // tile and the round trips match the last-arriver's; with more
+            // slices every slice's partial write, wait and second ticket
+            // cost more than the shared stores save
+            p.sk_band = cfg.split_reduce == SYMTILE_SPLIT_REDUCE_BANDED ||
+                        (cfg.split_reduce == SYMTILE_SPLIT_REDUCE_AUTO && fits && split == 2);
+        }
         p.role = cfg.variant == SYMTILE_FUSED_SEQ ? ROLE_FUSED : ROLE_LOCAL_ONLY;
         void* args[] = {&p};
         SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(64 * v->waves), args, 0, stream));

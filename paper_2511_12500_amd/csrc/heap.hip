@@ -254,8 +254,7 @@ int cu_count(int device) {
 // ack == i-1, writes the round's pattern into the reader's slot, waits for its
 // stores and publishes ready = i; the reader waits until ready == i, checks
 // every word, counts mismatches, and publishes ack = i in the writer's slot.
-// The data words are plain stores and loads, as the tile data of the GEMM
-// and copy kernels are.  How the counters publish and wait is the form:
+// The data words are plain loads, and plain stores except in the WT form.  How the counters publish and wait is the form:
 //   RELAXED  relaxed +1, relaxed polls, no fences: the unsynchronised form
 //            the protocol exists to prevent;
 //   FENCES   release fence at SCOPE then relaxed +1; relaxed polls then an
@@ -265,7 +264,18 @@ int cu_count(int device) {
 //            SCOPE) polls;
 //   CAS      the lock handshake of the workgroup-specialised listing:
 //            cas(i-1 -> i, release, SCOPE) publishes, cas(i -> i, acquire,
-//            SCOPE) polls until it observes i.
+//            SCOPE) polls until it observes i;
+//   WT       the data stored write-through (kStoreWriteThrough), released by
+//            the stores' acknowledgement alone (release_written_through, no
+//            L2 write-back), relaxed +1; relaxed polls then an acquire fence
+//            at SCOPE (the kernels' publication of write-through data);
+//   ACK      the same release after ordinary write-back stores: the control,
+//            which needs the write-back the fence performs;
+//   WT_COHERENT  WT's writer; the reader polls, then reads the data with
+//            coherent loads (kLoadCoherent) after acquire_coherent_reads, no
+//            acquire fence (the kernels' reads of published partials);
+//   WT_PLAIN WT's writer; the reader polls and reads with ordinary loads and
+//            no acquire fence: the control, which needs the L2 invalidate.
 // In RELAXED and FENCES the counters themselves are updated and polled at
 // agent scope or wider, so that only the data's ordering depends on SCOPE;
 // in RMW and CAS the counters take SCOPE too.  Compiler barriers keep
@@ -286,7 +296,12 @@ template <int SCOPE>
 __device__ bool mp_wait(int form, uint32_t* flag, uint32_t target, uint32_t spin_limit) {
     constexpr int WIDE = at_least_agent<SCOPE>();
     if (form == SYMTILE_MP_RELAXED) return symtile::flag_poll<WIDE>(flag, target, spin_limit);
-    if (form == SYMTILE_MP_FENCES) {
+    if (form == SYMTILE_MP_WT_COHERENT || form == SYMTILE_MP_WT_PLAIN) {
+        if (!symtile::flag_poll<WIDE>(flag, target, spin_limit)) return false;
+        if (form == SYMTILE_MP_WT_COHERENT) symtile::acquire_coherent_reads();
+        return true;
+    }
+    if (form == SYMTILE_MP_FENCES || form == SYMTILE_MP_WT || form == SYMTILE_MP_ACK) {
         if (!symtile::flag_poll<WIDE>(flag, target, spin_limit)) return false;
         symtile::fence_acquire<SCOPE>();
         return true;
@@ -311,6 +326,9 @@ __device__ void mp_publish(int form, uint32_t* flag, uint32_t i) {
     } else if (form == SYMTILE_MP_FENCES) {
         symtile::fence_release<SCOPE>();
         symtile::flag_signal<WIDE>(flag);
+    } else if (form == SYMTILE_MP_WT || form == SYMTILE_MP_ACK || form == SYMTILE_MP_WT_COHERENT ||
+               form == SYMTILE_MP_WT_PLAIN) {
+        symtile::flag_publish_written_through<WIDE>(flag);
     } else if (form == SYMTILE_MP_RMW) {
         symtile::atomic_add<__ATOMIC_RELEASE, SCOPE>(flag, 1u);
     } else {
@@ -350,11 +368,30 @@ __global__ __launch_bounds__(256) void litmus_mp_kernel(const uint64_t* bases, u
         __syncthreads();
         if (!s_ok) break;
         asm volatile("" ::: "memory");
-        if (writer) {
+        const bool wt = form == SYMTILE_MP_WT || form == SYMTILE_MP_WT_COHERENT ||
+                        form == SYMTILE_MP_WT_PLAIN;
+        if (writer && wt) {
+            const symtile::rsrc_t rd = symtile::make_rsrc(data, (uint32_t)words * 4u);
+            for (int j = tid; j < words; j += blockDim.x)
+                __builtin_amdgcn_raw_buffer_store_b32(litmus_word(i, j), rd, (uint32_t)j * 4u, 0,
+                                                      symtile::kStoreWriteThrough);
+            symtile::wg_stores_done();
+            if (tid == 0) mp_publish<SCOPE>(form, ready, (uint32_t)i);
+        } else if (writer) {
             for (int j = tid; j < words; j += blockDim.x)
                 *symtile::global_ptr(data + j) = litmus_word(i, j);
             symtile::wg_stores_done();
             if (tid == 0) mp_publish<SCOPE>(form, ready, (uint32_t)i);
+        } else if (form == SYMTILE_MP_WT_COHERENT) {
+            const symtile::rsrc_t rs = symtile::make_rsrc(data, (uint32_t)words * 4u);
+            uint32_t bad = 0;
+            for (int j = tid; j < words; j += blockDim.x)
+                bad += __builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)j * 4u, 0,
+                                                            symtile::kLoadCoherent) !=
+                       litmus_word(i, j);
+            if (bad) atomicAdd(&s_bad, bad);
+            __syncthreads();                 // every word read before the ack
+            if (tid == 0) mp_publish<SCOPE>(form, ack, (uint32_t)i);
         } else {
             uint32_t bad = 0;
             for (int j = tid; j < words; j += blockDim.x)
@@ -602,7 +639,7 @@ symtile_status symtile_litmus_mp(symtile_heap* h, size_t data_off, size_t flag_o
     if (symtile_status st = check_heap(h)) return st;
     if (pairs < 1 || pairs > 256 || rounds < 1 || words < 1 || words > (1 << 20))
         return symtile_host::fail(SYMTILE_EINVAL, "pairs in [1, 256], rounds >= 1, words in [1, 2^20]");
-    if (form < SYMTILE_MP_RELAXED || form > SYMTILE_MP_CAS)
+    if (form < SYMTILE_MP_RELAXED || form > SYMTILE_MP_WT_PLAIN)
         return symtile_host::fail(SYMTILE_EINVAL, "unknown message-passing form");
     if (scope < SYMTILE_SCOPE_BLOCK || scope > SYMTILE_SCOPE_SYS)
         return symtile_host::fail(SYMTILE_EINVAL, "unknown scope");

@@ -152,7 +152,10 @@ __global__ __launch_bounds__(kThreads) void tile_copy_kernel(const CopyParams p)
     // thread issuing them one after another into the same cache lines.
     symtile::wg_stores_done();
     if (threadIdx.x < 64) {
-        symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
+        if constexpr (POLICY == symtile::kStoreWriteThrough)
+            symtile::release_written_through();   // nothing of the run sits dirty in the L2
+        else
+            symtile::fence_release<__HIP_MEMORY_SCOPE_AGENT>();
         for (int it = first + (int)threadIdx.x; it < last; it += 64) {
             const int r = p.only_rank >= 0 ? p.only_rank : it / p.ntiles;
             int src, dst;

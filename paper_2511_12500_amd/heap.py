@@ -175,7 +175,7 @@ class GatheredOutput:
             gemm_wgs: int = 0, copy_wgs: int = 0, nontemporal: int = 0, group_m: int = 0,
             spin_limit: int = 0, epoch: int | None = None, stream: int | None = None,
             waves_per_wg: int = 0, trace: torch.Tensor | None = None,
-            copy_stream: int | None = None, split_k: int = 0) -> None:
+            copy_stream: int | None = None, split_k: int = 0, split_reduce: int = 0) -> None:
         """One call of rank ``rank`` (enqueued on the stream, asynchronous).
         For WG_SPEC, ``epoch`` (the value consumers wait for) defaults to one
         more than after the previous WG_SPEC call on these buffers.
@@ -184,7 +184,8 @@ class GatheredOutput:
         copy-kernel stream (default: one the heap creates).  ``split_k`` > 1
         (BULK_SYNC, FUSED_SEQ): each tile is computed as that many K slices,
         with this object's workspace; calls on one object that use split-K
-        must not overlap in time."""
+        must not overlap in time.  ``split_reduce``: SPLIT_REDUCE_AUTO (0),
+        SPLIT_REDUCE_LAST or SPLIT_REDUCE_BANDED (who sums the slices)."""
         if A.dtype != self.dtype or B_shard.dtype != self.dtype:
             raise TypeError("A and B_shard must have the output dtype")
         if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):
@@ -205,6 +206,7 @@ class GatheredOutput:
                           waves_per_wg=waves_per_wg, copy_stream=copy_stream,
                           trace=trace.data_ptr() if trace is not None else None)
         cfg.split_k = split_k
+        cfg.split_reduce = split_reduce
         ws = self.workspace(split_k) if split_k > 1 else None
         if ws is not None:               # None: no tiles, nothing to keep
             cfg.workspace, cfg.workspace_bytes = ws.data_ptr(), ws.numel()

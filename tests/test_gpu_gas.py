@@ -417,19 +417,22 @@ def test_padded_strides_on_tightly_sized_buffers():
             check_gathered(p, {rank: oracle_block_bounded(p.A, p.shards[rank], "bf16")})
 
 
-def test_split_k_timeout_then_stale_workspace_is_reported():
-    """A reducing slice allowed one poll gives up on the tiles whose partner
-    partial is not yet counted (ETIMEOUT at the barrier) and leaves their
-    counters as they are.  A later call on the same workspace, made without
-    zeroing it, reports the stale counters (EINVAL at the barrier) and writes
-    no stale sum; the Python wrapper zeroes the workspace after either report,
-    and its next call is exact."""
+@pytest.mark.parametrize("mode", [1, 2], ids=["last", "banded"])
+def test_split_k_timeout_then_stale_workspace_is_reported(mode):
+    """A slice allowed one poll gives up on the tiles whose partner partial
+    is not yet counted (ETIMEOUT at the barrier) and leaves their counters as
+    they are (last-arriver reduction: the two tickets; banded: the two first
+    tickets plus the second ticket of a slice that went on).  A later call on
+    the same workspace, made without zeroing it, reports the stale counters
+    (EINVAL at the barrier) and writes no stale sum; the Python wrapper
+    zeroes the workspace after either report, and its next call is exact."""
     pkg = sym()
     world, rank = 2, 0
     p = Problem(world, 1024, 512, 2048, "bf16", 64, 64, seed=17)     # 128 tiles x 2 slices
     want = {rank: oracle_block_bounded(p.A, p.shards[rank], "bf16")}
+    stale_ok = (0, 2) if mode == 1 else (0, 2, 3)
     p.sentinel()
-    p.run(rank, FUSED, split_k=2, spin_limit=1)
+    p.run(rank, FUSED, split_k=2, spin_limit=1, split_reduce=mode)
     try:
         p.heap.barrier()
         timed_out = False
@@ -443,7 +446,7 @@ def test_split_k_timeout_then_stale_workspace_is_reported():
     else:
         stale = _ws_counters(p).reshape(-1, 2)
         assert np.any(stale[:, 0] != 0)      # tickets left behind by the timed-out tiles
-        assert np.all((stale[:, 0] == 0) | (stale[:, 0] == 2))
+        assert np.all(np.isin(stale[:, 0], stale_ok)), np.unique(stale[:, 0])
         # the same workspace again, through the C ABI (no reset)
         ws = p.out.ws
         p.out.C_all().view(torch.int16).fill_(-1)
@@ -452,7 +455,8 @@ def test_split_k_timeout_then_stale_workspace_is_reported():
             p.heap.ptr(rank, p.out.flag_off), p.out.ready.data_ptr(), p.M, p.N, p.K, p.K, p.N,
             pkg.BF16, rank, world,
             pkg.GasConfig(variant=FUSED, tile_m=64, tile_n=64, split_k=2,
-                          workspace=ws.data_ptr(), workspace_bytes=ws.numel()),
+                          workspace=ws.data_ptr(), workspace_bytes=ws.numel(),
+                          split_reduce=mode),
             pkg.current_stream())
         with pytest.raises(pkg.SymtileError) as e:
             p.heap.barrier()
@@ -466,7 +470,7 @@ def test_split_k_timeout_then_stale_workspace_is_reported():
     p.sentinel()
     p.calls[:] = 0
     p.out.arrived_all().zero_()
-    p.run(rank, FUSED, split_k=2)
+    p.run(rank, FUSED, split_k=2, split_reduce=mode)
     p.barrier()
     check_gathered(p, want)
     assert np.all(_ws_counters(p) == 0)
@@ -658,6 +662,58 @@ def test_split_k_is_deterministic_across_grids(split):
             ref = got.copy()
         assert np.array_equal(got, ref), g
         assert np.all(_ws_counters(p) == 0)
+
+
+BANDED = [
+    # world, M, N_local, K, tile_m, tile_n, dtype, split_k
+    (2, 300, 136, 520, 128, 128, "bf16", 2),     # ragged M, N; two 64-row bands
+    (3, 1000, 520, 1000, 128, 128, "f16", 4),    # 32-row bands; the last tile row ragged
+    (4, 130, 264, 520, 256, 256, "bf16", 8),     # large accumulators: own rows via memory
+    (3, 300, 504, 200, 256, 224, "bf16", 2),     # 16x16x32 MFMA tile, 128-row bands
+    (2, 200, 72, 96, 64, 64, "f16", 2),          # 64x64 tile (4 waves), 32-row bands
+    (2, 512, 512, 2048, 256, 256, "f16", 2),     # large accumulators, two slices
+]
+
+
+@pytest.mark.parametrize("case", BANDED, ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_s%d" % c)
+def test_banded_split_reduce_matches_last_arriver_bitwise(case):
+    """The banded reduction (slice s sums and stores band s of the tile) and
+    the last-arriver reduction form the same slice-order sums: heaps equal
+    bit for bit, both against the oracle with the accumulation bound,
+    counters exact, workspace counters back at zero."""
+    pkg = sym()
+    world, M, N, K, tm, tn, dtype, split = case
+    rank = world - 1
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=21)
+    want = {rank: oracle_block_bounded(p.A, p.shards[rank], dtype)}
+    heaps = {}
+    for mode in (pkg.SPLIT_REDUCE_LAST, pkg.SPLIT_REDUCE_BANDED, pkg.SPLIT_REDUCE_BANDED):
+        p.sentinel()
+        p.run(rank, FUSED, split_k=split, split_reduce=mode)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[rank]))
+        assert np.all(_ws_counters(p) == 0), mode
+        got = u16(p.out.C_all())
+        if heaps:
+            assert np.array_equal(got, next(iter(heaps.values()))), mode
+        heaps[mode] = got
+
+
+def test_banded_split_reduce_argument_errors():
+    """BANDED needs one resident workgroup per slice and whole bands;
+    otherwise EUNSUPPORTED (AUTO falls back to the last-arriver reduction)."""
+    pkg = sym()
+    p = Problem(2, 300, 136, 520, "bf16", 128, 128, seed=22)
+    for kw in (dict(split_k=3), dict(split_k=2, gemm_wgs=5), dict(split_k=8)):
+        with pytest.raises(pkg.SymtileError, match="EUNSUPPORTED"):
+            p.out.run(p.dA, p.dB[0], 0, FUSED, split_reduce=pkg.SPLIT_REDUCE_BANDED, **kw)
+    with pytest.raises(pkg.SymtileError, match="EINVAL"):
+        p.out.run(p.dA, p.dB[0], 0, FUSED, split_k=2, split_reduce=3)
+    want = {0: oracle_block(p.A, p.shards[0], "bf16")}
+    p.sentinel()
+    p.run(0, FUSED, split_k=3)                     # AUTO: 128 rows do not split in 3 bands
+    p.barrier()
+    check_gathered(p, want)
 
 
 def test_split_k_two_slices_match_one_within_rounding():

@@ -402,6 +402,58 @@ def test_litmus_message_passing_release_acquire_sees_every_word(form, scope):
     assert bad == 0
 
 
+@pytest.mark.parametrize("scope", ["gpu", "sys"])
+def test_litmus_write_through_release_sees_every_word(scope):
+    """The kernels' publication of write-through data: the writer stores the
+    round write-through, waits for the stores' acknowledgement and adds to
+    the counter with no L2 write-back; the reader polls and acquires.  No
+    reader on another XCD ever sees a word of an older round."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, done, timed_out = _litmus(pkg, heap, 32, 300, 2048, "wt", scope)
+    assert not timed_out
+    assert done == 32 * 300
+    assert bad == 0
+
+
+@pytest.mark.parametrize("scope", ["gpu", "sys"])
+def test_litmus_coherent_reads_without_invalidate_see_every_word(scope):
+    """Write-through publication read back with coherent loads: the reader
+    polls the counter and reads the round with coherent (sc0 sc1) loads, with
+    no acquire fence; no reader ever sees a word of an older round."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, done, timed_out = _litmus(pkg, heap, 32, 300, 2048, "wt_coherent", scope)
+    assert not timed_out
+    assert done == 32 * 300
+    assert bad == 0
+
+
+def test_litmus_plain_reads_without_invalidate_are_reported():
+    """The control of the coherent-read form: ordinary loads with no acquire
+    fence may hit the reader's own L2 copy of an older round.  No guarantee;
+    every round must complete, and the stale-word count is reported."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, done, timed_out = _litmus(pkg, heap, 32, 300, 2048, "wt_plain")
+    assert not timed_out and done == 32 * 300
+    print(f"write-through data read with ordinary loads, no acquire: {bad} stale words of "
+          f"{32 * 300 * 2048}")
+
+
+def test_litmus_ack_only_release_of_write_back_stores_is_reported():
+    """The control of the write-through form: the same acknowledgement-only
+    release after ordinary (write-back) stores, which may still sit dirty in
+    the writer's L2.  No guarantee; the test requires that every round
+    completes and reports the stale-word count."""
+    pkg = sym()
+    heap = pkg.Heap(8, 16 << 20)
+    bad, done, timed_out = _litmus(pkg, heap, 32, 300, 2048, "ack")
+    assert not timed_out and done == 32 * 300
+    print(f"acknowledgement-only release of write-back stores: {bad} stale words of "
+          f"{32 * 300 * 2048}")
+
+
 def test_litmus_relaxed_form_terminates():
     """Without release and acquire the protocol gives no guarantee; the test
     only requires that every round completes (the stale-word count is
@@ -471,7 +523,7 @@ def test_litmus_rejects_bad_arguments():
     res = torch.zeros(2, dtype=torch.int32, device="cuda")
     for args, name in (((data, flags, 0, 1, 16, 1, 1), "EINVAL"),       # no pairs
                        ((data, data, 1, 1, 16, 1, 1), "EINVAL"),        # flags overlap data
-                       ((data, flags, 1, 1, 16, 4, 1), "EINVAL"),       # unknown form
+                       ((data, flags, 1, 1, 16, 8, 1), "EINVAL"),       # unknown form
                        ((data, flags, 1, 1, 16, 1, 3), "EINVAL"),       # unknown scope
                        ((data, flags, 256, 1, 4, 1, 1), "EUNSUPPORTED")):  # 512 WGs > CUs
         with pytest.raises(pkg.SymtileError) as e:

@@ -248,3 +248,117 @@ def test_timeout_model_finds_the_planted_errors():
         _timeout_then_next_call(1, 2, 2, 2, reset_on_timeout=True)
     with pytest.raises(AssertionError, match="neither reduced nor reported"):
         _timeout_then_next_call(1, 2, 2, 2, check_tickets=False)
+
+
+# ---------------------------------------------------------------------------
+# Banded reduction.  With one resident workgroup per slice, the tile's rows
+# form S bands and every slice reduces and stores one of them:
+#
+#   ticket = cnt[t]++                     (ticket >= S: stale workspace, skip)
+#   write the partial rows of the other bands ; written[t]++   (after a release)
+#   wait written[t] >= S ; read the other slices' partials of band s
+#   store band s ; u = cnt[t]++           (after a release)
+#   if u == 2S-1: acquire, cnt[t] = written[t] = 0, publish the tile's counters
+#
+# Every slice waits for all the others, so the protocol needs them resident
+# together; the host chooses it only when every unit has a workgroup of its
+# own and the grid fits on the device at once.
+
+B_START, B_WRITE, B_COUNT, B_WAIT, B_READ, B_STORE, B_TICKET2, B_PUBLISH, B_DONE = range(9)
+
+
+def _explore_banded(T: int, S: int, R: int, wait_target: int | None = None,
+                    publish_ticket: int | None = None) -> int:
+    """Every interleaving of T tiles x S slices, one workgroup per slice, at
+    most R resident at once.  Returns the number of terminal paths."""
+    target = S if wait_target is None else wait_target
+    last = 2 * S - 1 if publish_ticket is None else publish_ticket
+    G = T * S
+    full = (1 << S) - 1
+
+    @lru_cache(maxsize=None)
+    def reachable(state) -> int:
+        pcs, resident, cnt, written, parts, stored, published = state
+        if all(pc == B_DONE for pc in pcs):
+            assert all(c == 0 for c in cnt) and all(w == 0 for w in written), "counters left"
+            assert all(p == 1 for p in published), f"tiles published {published}"
+            return 1
+        moves = []
+        if len(resident) < R:
+            for g in range(G):
+                if g not in resident and pcs[g] == B_START:
+                    moves.append(("admit", g))
+        for g in resident:
+            t = g // S
+            if pcs[g] == B_WAIT and written[t] < target:
+                continue
+            moves.append(("step", g))
+        assert moves, f"deadlock in {state}"
+        total = 0
+        for kind, g in moves:
+            pc, res = list(pcs), list(resident)
+            c, wr, pa, st, pb = list(cnt), list(written), list(parts), list(stored), list(published)
+            if kind == "admit":
+                res.append(g)
+            else:
+                t, s = divmod(g, S)
+                p = pc[g]
+                if p == B_START:
+                    ticket = c[t]
+                    c[t] += 1
+                    assert ticket < S, "first-round ticket past the slice count"
+                    pc[g] = B_WRITE
+                elif p == B_WRITE:
+                    pa[t] |= 1 << s
+                    pc[g] = B_COUNT
+                elif p == B_COUNT:
+                    wr[t] += 1
+                    pc[g] = B_WAIT
+                elif p == B_WAIT:
+                    pc[g] = B_READ
+                elif p == B_READ:
+                    assert pa[t] == full, "a band summed before every partial was written"
+                    pc[g] = B_STORE
+                elif p == B_STORE:
+                    st[t] |= 1 << s
+                    pc[g] = B_TICKET2
+                elif p == B_TICKET2:
+                    u = c[t]
+                    c[t] += 1
+                    pc[g] = B_PUBLISH if u == last else B_DONE
+                elif p == B_PUBLISH:
+                    assert st[t] == full, "tile published before every band was stored"
+                    c[t] = wr[t] = 0
+                    pb[t] += 1
+                    pc[g] = B_DONE
+                if pc[g] == B_DONE:
+                    res.remove(g)
+            total += reachable((tuple(pc), tuple(res), tuple(c), tuple(wr), tuple(pa),
+                                tuple(st), tuple(pb)))
+        return total
+
+    init = ((B_START,) * G, (), (0,) * T, (0,) * T, (0,) * T, (0,) * T, (0,) * T)
+    n = reachable(init)
+    reachable.cache_clear()
+    return n
+
+
+@pytest.mark.parametrize("T,S", [(1, 2), (1, 3), (1, 4), (2, 2)])
+def test_banded_protocol_all_resident_publishes_once(T, S):
+    assert _explore_banded(T, S, R=T * S) >= 1
+
+
+def test_banded_model_finds_the_planted_errors():
+    """Pins of the banded model: without co-residency it deadlocks (which is
+    why the host requires one resident workgroup per slice); waiting for S-1
+    counts lets a slice sum a band before the last partial is written;
+    publishing on the second-to-last ticket publishes a tile with a band
+    missing."""
+    with pytest.raises(AssertionError, match="deadlock"):
+        _explore_banded(1, 2, R=1)
+    with pytest.raises(AssertionError, match="deadlock"):
+        _explore_banded(1, 3, R=2)
+    with pytest.raises(AssertionError, match="before every partial"):
+        _explore_banded(1, 2, R=2, wait_target=1)
+    with pytest.raises(AssertionError, match="before every band|counters left|published"):
+        _explore_banded(1, 2, R=2, publish_ticket=2)
