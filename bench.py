@@ -82,6 +82,8 @@ def gas_profile_name(args, wl) -> str:
     configuration (workload, schedule, tile, store policy, producer/consumer
     split, K slices)."""
     sk = f"_k{args.split_k}" if args.split_k > 1 else ""
+    if args.split_k > 1 and getattr(args, "split_reduce", 0):
+        sk += f"_r{args.split_reduce}"
     if (args.variant, args.tile, args.nontemporal, args.gemm_wgs, args.copy_wgs,
             args.group_m, sk) == ("fused_seq", "256x256", 2, 0, 0, 0, ""):
         return f"gas_kernel_{wl.name}.md"
@@ -119,6 +121,9 @@ def parse_args(argv=None):
     ap.add_argument("--group-m", type=int, default=0)
     ap.add_argument("--split-k", type=int, default=0,
                     help="K slices per output tile (bulk_sync, fused_seq; 0 or 1 = none)")
+    ap.add_argument("--split-reduce", type=int, default=0,
+                    help="who sums the K slices: 0 auto, 1 the last slice, 2 banded (every slice "
+                         "sums and stores one band of rows)")
     ap.add_argument("--nontemporal", type=int, default=2,
                     help="output store policy: 0 default, 1 non-temporal, 2 write-through")
     ap.add_argument("--copy-tile", type=int, default=128)
@@ -138,29 +143,31 @@ def parse_args(argv=None):
 VARIANTS = ("bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec")
 
 # The configs array: (workload, schedule, tile, K slices, producer WGs,
-# consumer WGs).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256)
+# consumer WGs, split-K reduction: 0 auto, 1 last slice, 2 banded).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256)
 # is not repeated here.
 SWEEP = [
-    ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0),
-    ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0),
-    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0),
-    ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0),
-    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0),
-    ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wave_spec", "256x128", 0, 0, 0),
-    ("gas_bf16_w8_m4096_k8192_n3584", "unfused_pc", "256x256", 0, 224, 32),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 248, 8),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 240, 16),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 224, 32),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 208, 48),
-    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 192, 64),
-    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x256", 2, 0, 0),
-    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x128", 0, 0, 0),
-    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x256", 2, 0, 0),
-    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x128", 0, 0, 0),
-    ("gas_f16_w8_m8192_k8192_n1024", "wave_spec", "256x128", 0, 0, 0),
-    ("gas_f16_w8_m8192_k8192_n1024", "wg_spec", "256x128", 0, 128, 128),
-    ("gas_f16_w8_m8192_k8192_n1024", "unfused_pc", "256x128", 0, 192, 64),
+    ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0, 0),
+    ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 2),
+    ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0, 0),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wave_spec", "256x128", 0, 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "unfused_pc", "256x256", 0, 224, 32, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 248, 8, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 240, 16, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 224, 32, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 208, 48, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "wg_spec", "256x256", 0, 192, 64, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x256", 2, 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x256", 2, 0, 0, 1),
+    ("gas_f16_w8_m8192_k8192_n1024", "fused_seq", "256x128", 0, 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x256", 2, 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "bulk_sync", "256x128", 0, 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "wave_spec", "256x128", 0, 0, 0, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "wg_spec", "256x128", 0, 128, 128, 0),
+    ("gas_f16_w8_m8192_k8192_n1024", "unfused_pc", "256x128", 0, 192, 64, 0),
 ]
 
 
@@ -229,13 +236,13 @@ def per_call_median_ms(launch, torch, n: int) -> float:
 
 
 def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps, warmup,
-            label_args, with_median=False) -> dict:
+            label_args, with_median=False, split_reduce=0) -> dict:
     """One timed GEMM + All-Scatter configuration on `case`."""
     wl = case.wl
     v = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
          "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[variant]
     kw = dict(gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, nontemporal=args.nontemporal,
-              group_m=args.group_m, split_k=split_k)
+              group_m=args.group_m, split_k=split_k, split_reduce=split_reduce)
 
     def launch():
         case.out.run(case.dA, case.dB, 0, v, **kw)
@@ -273,8 +280,9 @@ def gemm_bytes(wl) -> int:
 class _Label:
     """The argument names gas_profile_name reads, for a configs entry."""
 
-    def __init__(self, args, variant, tile, split_k, gemm_wgs, copy_wgs):
+    def __init__(self, args, variant, tile, split_k, gemm_wgs, copy_wgs, split_reduce=0):
         self.variant, self.tile, self.split_k = variant, tile, split_k
+        self.split_reduce = split_reduce
         self.gemm_wgs, self.copy_wgs = gemm_wgs, copy_wgs
         self.nontemporal, self.group_m = args.nontemporal, args.group_m
 
@@ -285,7 +293,8 @@ def bench_gas(args, torch, sym, workload):
         args.tile = "256x128" if args.variant == "wave_spec" else "256x256"
     case = GasCase(torch, sym, workload, wl, args.tile)
     r = gas_leg(args, torch, sym, case, args.variant, args.split_k, args.gemm_wgs,
-                args.copy_wgs, args.steps, args.warmup, args, with_median=True)
+                args.copy_wgs, args.steps, args.warmup, args, with_median=True,
+                split_reduce=args.split_reduce)
     res = {
         "value": r["tflops"],
         "ms_per_step": r["ms"],
@@ -296,7 +305,7 @@ def bench_gas(args, torch, sym, workload):
                    "world_size": wl.world, "rank": 0, "N_gathered": wl.N_gathered,
                    "variant": args.variant, "tile": args.tile, "gemm_wgs": args.gemm_wgs,
                    "copy_wgs": args.copy_wgs, "nontemporal": args.nontemporal,
-                   "split_k": max(args.split_k, 1)},
+                   "split_k": max(args.split_k, 1), "split_reduce": args.split_reduce},
         "dtype": wl.dtype,
     }
     A, B = case.A, case.B
@@ -309,18 +318,20 @@ def bench_sweep(args, torch, sym, workload) -> list:
     built once."""
     out = []
     cases = {}
-    for name, variant, tile, split_k, g, c in SWEEP:
+    for name, variant, tile, split_k, g, c, red in SWEEP:
         key = (name, tile)
         if key not in cases:
             for k in list(cases):
                 cases.pop(k).close()
             cases[key] = GasCase(torch, sym, workload, workload.GEMM_WORKLOADS[name], tile)
         case = cases[key]
-        label = _Label(args, variant, tile, split_k, g, c)
-        r = gas_leg(args, torch, sym, case, variant, split_k, g, c, args.sweep_steps, 5, label)
+        label = _Label(args, variant, tile, split_k, g, c, red)
+        r = gas_leg(args, torch, sym, case, variant, split_k, g, c, args.sweep_steps, 5, label,
+                    split_reduce=red)
         wl = case.wl
         out.append({"workload": name, "dtype": wl.dtype, "schedule": variant, "tile": tile,
-                    "split_k": max(split_k, 1), "gemm_wgs": g, "copy_wgs": c,
+                    "split_k": max(split_k, 1), "split_reduce": red, "gemm_wgs": g,
+                    "copy_wgs": c,
                     "ms": r["ms"], "value": r["tflops"], "unit": "TFLOP/s",
                     "steps": args.sweep_steps, "settle": r["settle"],
                     "roofline": r["roofline"]})
