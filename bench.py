@@ -415,26 +415,32 @@ def bench_copy(args, torch, sym, workload, tile=None):
 
 
 def cpu_model() -> str:
-    """The host CPU's full model name (lscpu, else /proc/cpuinfo), with the
-    socket count."""
+    """The host CPU as the OS reports it: the model name (the longer of
+    lscpu's and /proc/cpuinfo's), the family / model / stepping numbers, the
+    sockets, and the logical CPUs this process may use."""
     import subprocess
+    info = {}
     try:
         out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
-        info = dict(l.split(":", 1) for l in out.splitlines() if ":" in l)
-        name = info.get("Model name", "").strip()
-        if name:
-            sockets = info.get("Socket(s)", "").strip()
-            return name + (f" ({sockets} sockets)" if sockets else "")
+        info = {k.strip(): v.strip() for k, v in
+                (l.split(":", 1) for l in out.splitlines() if ":" in l)}
     except (OSError, subprocess.SubprocessError, ValueError):
         pass
+    names = [info.get("Model name", "")]
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
                 if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                    names.append(line.split(":", 1)[1].strip())
+                    break
     except OSError:
         pass
-    return "unknown"
+    name = max(names, key=len) or "unknown"
+    ids = [f"{k.lower()} {info[k]}" for k in ("CPU family", "Model", "Stepping")
+           if info.get(k)]
+    extra = ids + ([f"{info['Socket(s)']} socket(s)"] if info.get("Socket(s)") else [])
+    extra.append(f"{len(os.sched_getaffinity(0))} logical CPUs available")
+    return f"{name} ({', '.join(extra)})"
 
 
 def oracle_threads() -> int:
