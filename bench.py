@@ -57,8 +57,9 @@ def sources_sha(paths) -> str:
 def counter_traffic(name: str, sources) -> float | None:
     """HBM bytes per launch from a committed rocprofv3 --pmc summary
     ``profiles/<name>`` (written by ``python -m paper_2511_12500_amd.profiling``):
-    lines ``- bytes_per_dispatch: X`` and ``- source_sha: H``.  None when absent
-    or when the kernel source changed since the counters were taken."""
+    lines ``- bytes_per_dispatch: X`` (``- bytes_per_call: X`` for a call of
+    several kernels) and ``- source_sha: H``.  None when absent or when the
+    kernel source changed since the counters were taken."""
     path = os.path.join(PROFILES, name)
     if not os.path.exists(path):
         return None
@@ -72,7 +73,7 @@ def counter_traffic(name: str, sources) -> float | None:
     if fields.get("source_sha") != sources_sha(sources):
         return None
     try:
-        return float(fields["bytes_per_dispatch"])
+        return float(fields.get("bytes_per_call", fields["bytes_per_dispatch"]))
     except (KeyError, ValueError):
         return None
 
@@ -123,7 +124,7 @@ def parse_args(argv=None):
                     help="K slices per output tile (bulk_sync, fused_seq; 0 or 1 = none)")
     ap.add_argument("--split-reduce", type=int, default=0,
                     help="who sums the K slices: 0 auto, 1 the last slice, 2 banded (every slice "
-                         "sums and stores one band of rows)")
+                         "sums and stores one band of rows), 3 a second reduction kernel")
     ap.add_argument("--nontemporal", type=int, default=2,
                     help="output store policy: 0 default, 1 non-temporal, 2 write-through")
     ap.add_argument("--copy-tile", type=int, default=128)
@@ -143,13 +144,14 @@ def parse_args(argv=None):
 VARIANTS = ("bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec")
 
 # The configs array: (workload, schedule, tile, K slices, producer WGs,
-# consumer WGs, split-K reduction: 0 auto, 1 last slice, 2 banded).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256)
-# is not repeated here.
+# consumer WGs, split-K reduction: 0 auto, 1 last slice, 2 banded, 3 reduction
+# kernel).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256) is not
+# repeated here.
 SWEEP = [
     ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0, 0),
     ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0, 0),
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 0),
-    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 2),
+    ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 1),
     ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0, 0),
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0, 0),
     ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0, 0),

@@ -131,15 +131,23 @@ typedef struct {
                              (tiles * split_k <= symtile_device_info's
                              max_coresident_wgs, gemm_wgs 0 or tiles * split_k) and
                              tile_m / split_k a multiple of 32 (16 for 256x224),
-                             else EUNSUPPORTED.  0 = BANDED where it applies and
-                             split_k = 2, else LAST.  Both give the same bits. */
+                             else EUNSUPPORTED.
+                             SYMTILE_SPLIT_REDUCE_KERNEL: every slice writes its
+                             partial and a second kernel on the same stream sums
+                             each tile's rows in bands spread over the CUs and
+                             stores them (any grid); gemm_wgs sizes the first
+                             kernel only.
+                             0 = for split_k = 2 BANDED where it applies, else
+                             LAST; for split_k > 2 KERNEL.  All give the same
+                             bits. */
 } symtile_gas_config;
 
 /* Reduction of split-K slices (symtile_gas_config.split_reduce). */
 typedef enum {
     SYMTILE_SPLIT_REDUCE_AUTO = 0,
     SYMTILE_SPLIT_REDUCE_LAST = 1,
-    SYMTILE_SPLIT_REDUCE_BANDED = 2
+    SYMTILE_SPLIT_REDUCE_BANDED = 2,
+    SYMTILE_SPLIT_REDUCE_KERNEL = 3
 } symtile_split_reduce;
 
 /* Per-tile trace record.  Times are ticks of the device's constant-rate

@@ -507,9 +507,10 @@ __device__ __forceinline__ uint64_t trace_location() {
 
 // Device error word codes (OR-ed into the heap's error word).
 //   ERR_TIMEOUT    a bounded wait expired;
-//   ERR_WORKSPACE  a split-K slice drew an arrival ticket beyond the slice
-//                  count: the workspace counters were not zero when the call
-//                  started (a timed-out call leaves them so).
+//   ERR_WORKSPACE  a split-K slice (or band of the reduction kernel) drew a
+//                  ticket beyond its count, or found the other counter
+//                  non-zero: the workspace counters were not zero when the
+//                  call started (a timed-out call leaves them so).
 enum : uint32_t { ERR_TIMEOUT = 1u, ERR_WORKSPACE = 2u };
 
 __device__ __forceinline__ void raise_error(uint32_t* err, uint32_t code) {

@@ -11,7 +11,7 @@ itself imports without the library, so a fresh checkout can build it.
 _BINDING = (
     "ATOMIC_OPS", "BF16", "BULK_SYNC", "F16", "F32", "FUSED_SEQ", "GET", "LIB_PATH", "LOAD",
     "PUT", "SCOPES", "SEMS", "STORE", "MP_FORMS", "SB_FORMS", "symtile_litmus_sb",
-    "SPLIT_REDUCE_AUTO", "SPLIT_REDUCE_LAST", "SPLIT_REDUCE_BANDED",
+    "SPLIT_REDUCE_AUTO", "SPLIT_REDUCE_LAST", "SPLIT_REDUCE_BANDED", "SPLIT_REDUCE_KERNEL",
     "TRACE_WORDS", "UNFUSED_PC", "WAVE_SPEC", "WG_SPEC", "GasConfig", "SymtileError", "lib", "symtile_atomic_exercise",
     "symtile_barrier", "symtile_clock_rate_khz", "symtile_device_info",
     "symtile_gas_workspace_bytes", "symtile_gemm_all_scatter",

@@ -9,7 +9,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsymtile.
 
 F16, BF16, F32 = 1, 2, 3
 BULK_SYNC, FUSED_SEQ, WG_SPEC, UNFUSED_PC, WAVE_SPEC = 0, 1, 2, 3, 4
-SPLIT_REDUCE_AUTO, SPLIT_REDUCE_LAST, SPLIT_REDUCE_BANDED = 0, 1, 2
+SPLIT_REDUCE_AUTO, SPLIT_REDUCE_LAST, SPLIT_REDUCE_BANDED, SPLIT_REDUCE_KERNEL = 0, 1, 2, 3
 PUT, GET = 0, 1
 LOAD, STORE = 0, 1
 ATOMIC_OPS = {"add": 0, "xchg": 1, "cas": 2, "and": 3, "or": 4, "xor": 5, "min": 6, "max": 7}

@@ -64,8 +64,12 @@ constexpr int kRowBytes = BK * 2;      // LDS bytes per staged A row (4 chunks o
 constexpr int NS = 4;                  // pipeline stages (LDS ring)
 constexpr int PD = 3;                  // prefetch distance in stages (< NS)
 
-enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2, ROLE_WAVE_SPEC = 3 };
-// (UNFUSED_PC runs gas_kernel as WG_SPEC producers only, and consumer_kernel.)
+enum KernelRole : int { ROLE_LOCAL_ONLY = 0, ROLE_FUSED = 1, ROLE_WG_SPEC = 2, ROLE_WAVE_SPEC = 3,
+                        ROLE_REDUCE = 4 };
+// (UNFUSED_PC runs gas_kernel as WG_SPEC producers only, and consumer_kernel.
+// ROLE_REDUCE runs gas_kernel<..., RED = true>, the second kernel of the
+// split-K reduction-kernel mode: no K loop, unit = (tile, band of rows), the
+// band's sum of the partials, then the epilogue.)
 
 struct GasParams {
     const uint16_t* A;
@@ -92,8 +96,12 @@ struct GasParams {
     float* sk_part;         // [num_tiles][split][BM*BN] fp32 partial tiles
     // Banded reduction (every unit has its own co-resident workgroup): slice
     // s sums and stores tile rows [s*BM/split, (s+1)*BM/split); 0 = the last
-    // slice to arrive sums and stores the whole tile.
+    // slice to arrive sums and stores the whole tile; 2 = every slice only
+    // writes its partial (the first kernel of the reduction-kernel mode).
     int sk_band;
+    // ROLE_REDUCE: bands of rows per tile (units = tiles * reduce_bands), and
+    // whether the tile goes to every slot (fused) or the local one (bulk).
+    int reduce_bands, reduce_all;
 };
 
 // Trace record of tile (tm, tn), or nullptr when tracing is off.
@@ -488,7 +496,7 @@ __device__ void copy_wave_tiles(const GasParams& p, int KT) {
 // staged columns past BN are loaded but never read.  With NW = 8 two waves
 // share each SIMD, so one wave's MFMAs run while the other waits on LDS,
 // global loads or the barrier.
-template <int BM, int BN, bool BF16, int NW, int MF, bool CW = false>
+template <int BM, int BN, bool BF16, int NW, int MF, bool CW = false, bool RED = false>
 __global__ __launch_bounds__(64 * (NW + CW))
 __attribute__((amdgpu_waves_per_eu(NW / 4 + CW, NW / 4 + CW)))
 void gas_kernel(const GasParams p) {
@@ -572,15 +580,26 @@ void gas_kernel(const GasParams p) {
     const int tr_row = ((MF == 32) ? 8 * (lane >> 5) : 8 * (lane >> 4)) + ((lane & 15) >> 2);
     const int tr_col = ((MF == 32) ? 16 * ((lane >> 4) & 1) : 0) + 4 * (lane & 3);
 
+    // (the reduction kernel is an instantiation of its own, so its code
+    // leaves the register allocation of the K-loop kernels alone)
+    constexpr bool reducer = RED;
     for (int t = pid; t < p.units; t += G) {
         int tm, tn, ks;
-        unit_coords(t, G, p, tm, tn, ks);
+        if (reducer) {
+            // unit = (tile, band); ks is the band (no K slice: KT = 0 below)
+            const int tile = t / p.reduce_bands;
+            ks = t - tile * p.reduce_bands;
+            tm = tile / p.tiles_n;
+            tn = tile - tm * p.tiles_n;
+        } else {
+            unit_coords(t, G, p, tm, tn, ks);
+        }
         // this unit's K slice: stages [kt0, kt0 + KT)
-        const int kt0 = ks * KT_all / p.split;
-        const int KT = (ks + 1) * KT_all / p.split - kt0;
+        const int kt0 = reducer ? 0 : ks * KT_all / p.split;
+        const int KT = reducer ? 0 : (ks + 1) * KT_all / p.split - kt0;
         // (the trace record's address is recomputed at each event so that
         // nothing extra stays live across the K loop)
-        if (p.trace && tid == 0 && ks == 0) {
+        if (p.trace && tid == 0 && ks == 0 && !reducer) {
             uint64_t* tr = tile_trace(p, tm, tn);
             tr[SYMTILE_TRACE_START] = symtile::clock_now();
             tr[SYMTILE_TRACE_WHERE] = symtile::trace_location();
@@ -779,7 +798,7 @@ void gas_kernel(const GasParams p) {
             mfmas1();              // last stage, group 1
         }
         __syncthreads();           // every wave is done with the ring
-        if (p.trace && tid == 0 && ks == 0)
+        if (p.trace && tid == 0 && ks == 0 && !reducer)
             tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
 
         // ---- split-K: combine the K slices of the tile ------------------
@@ -803,18 +822,22 @@ void gas_kernel(const GasParams p) {
         // the same bits, whichever slice came last.  (Not built into the
         // copy-wave kernel: wave specialisation has no split-K, and its
         // third wave per SIMD leaves no registers for it.)
-        const bool banded = !CW && p.split > 1 && p.sk_band != 0;
-        const int band_rows = banded ? BM / p.split : BM;
+        const bool banded = !CW && p.split > 1 &&
+                            (reducer ? p.reduce_bands > 1 : p.sk_band == 1);
+        const int band_rows = banded ? BM / (reducer ? p.reduce_bands : p.split) : BM;
         // band of accumulator block row i of this wave (blocks are MF rows)
         auto block_band = [&](int i) { return (wm * WM + i * MF) / band_rows; };
         if (!CW && p.split > 1) {
             __shared__ uint32_t s_ticket, s_ok;
             const int tile = tm * p.tiles_n + tn;
             uint32_t* cnt = p.sk_cnt + 2 * tile;
-            if (tid == 0)
+            // (the reduction-kernel mode takes no ticket: the kernel boundary
+            // orders its two kernels)
+            const bool ticketed = !reducer && p.sk_band != 2;
+            if (tid == 0 && ticketed)
                 s_ticket = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
             __syncthreads();
-            const uint32_t ticket = __builtin_amdgcn_readfirstlane(s_ticket);
+            const uint32_t ticket = ticketed ? __builtin_amdgcn_readfirstlane(s_ticket) : 0u;
             if (ticket >= (uint32_t)p.split) {
                 // more arrivals than slices: the counters were not zero at
                 // the start of this call (a timed-out call leaves them so);
@@ -822,7 +845,7 @@ void gas_kernel(const GasParams p) {
                 if (tid == 0) symtile::raise_error(p.err, symtile::ERR_WORKSPACE);
                 continue;
             }
-            const bool last = !banded && ticket + 1 == (uint32_t)p.split;
+            const bool last = !banded && ticketed && ticket + 1 == (uint32_t)p.split;
             // Partial tile of slice q: each thread's accumulators, 16 bytes
             // per (i, j, 4-value group), so a wave's access is 1 KiB contiguous.
             auto slot = [&](int q) {
@@ -893,79 +916,153 @@ void gas_kernel(const GasParams p) {
                     __builtin_amdgcn_sched_barrier(0);
                 }
             };
-            // 1. partials: every slice but the last-arriving one (banded:
-            // every slice, for the other bands' rows), and the reducing
-            // slice's own rows when it sums from memory
-            if (!last || own_to_memory) put_partial(ks);
-            if (!last) {
-                symtile::wg_stores_done();
-                // (partials are always stored write-through)
-                if (tid == 0) symtile::flag_publish_written_through(cnt + 1);
-                if (!banded) continue;
-            } else if (own_to_memory) {
-                __builtin_amdgcn_s_waitcnt(vm_wait(0));
-            }
-            // 2. wait for the others' partials (bounded); they were written
-            // through and are read with coherent loads, so the wait needs
-            // no L2 invalidate
-            if (tid == 0) {
-                const uint32_t target = banded ? (uint32_t)p.split : (uint32_t)p.split - 1;
-                const bool ok = symtile::flag_wait_coherent(cnt + 1, target, p.spin_limit);
-                if (ok && !banded) {
-                    // every slice of this call has counted itself: the next
-                    // call starts again from zero (banded: reset by the last
-                    // slice to store its band, below)
-                    symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
-                    symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
-                } else if (!ok) {
-                    // a slice that holds a ticket may still count itself
-                    // later, so the counters are left as they are: the next
-                    // call that uses this workspace then draws tickets past
-                    // the slice count and reports ERR_WORKSPACE instead of
-                    // summing stale partials, until the caller zeroes them
-                    symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+            if constexpr (RED) {
+                // Second kernel: this band's p0 + p1 + ... in slice order,
+                // rounded straight into the LDS staging of the epilogue (the
+                // first kernel's partials were completed by the kernel
+                // boundary).  Every wave shares the band: chunk x is 16 bytes
+                // of a partial (4 consecutive columns of one row), taken in
+                // memory order, so a wave reads 1 KiB runs; CH chunks of QB
+                // slices are in flight per thread at once.
+                constexpr int GPA = ACC_N / 4;
+                constexpr int PER_BR = NI * GPA * WGN * 64;    // chunks per block row
+                constexpr int CH = 4, QB = 4;
+                const int total = band_rows / MF * PER_BR;
+                const int br0 = ks * (band_rows / MF);
+                uint8_t* Cs = smem;
+#pragma unroll 1
+                for (int x0 = 0; x0 < total; x0 += THREADS * CH) {
+                    float sum[CH][4];
+#pragma unroll 1
+                    for (int q0 = 0; q0 < p.split; q0 += QB) {
+                        symtile::u32x4 v[CH][QB];
+#pragma unroll
+                        for (int c = 0; c < CH; ++c) {
+                            const int x = x0 + c * THREADS + tid;
+                            const int br = br0 + x / PER_BR, rem = x % PER_BR;
+                            const int jg = rem / (WGN * 64), wl = rem % (WGN * 64);
+                            const uint32_t off =
+                                (uint32_t)(((((br % MI) * NI + jg / GPA) * GPA + jg % GPA) * THREADS +
+                                            ((br / MI) * WGN + wl / 64) * 64 + wl % 64) * 16);
+#pragma unroll
+                            for (int qq = 0; qq < QB; ++qq) {
+                                const int q = min(q0 + qq, p.split - 1);
+                                v[c][qq] = symtile::buf_ld16p<symtile::kLoadCoherent>(
+                                    slot(q), x < total && q0 + qq < p.split ? off : symtile::kOOB, 0);
+                            }
+                        }
+#pragma unroll
+                        for (int c = 0; c < CH; ++c)
+#pragma unroll
+                            for (int qq = 0; qq < QB; ++qq) {
+                                if (q0 + qq >= p.split) continue;      // uniform
+                                const f32x4_t y = __builtin_bit_cast(f32x4_t, v[c][qq]);
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    sum[c][e] = q0 + qq == 0 ? y[e] : sum[c][e] + y[e];
+                            }
+                    }
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) {
+                        const int x = x0 + c * THREADS + tid;
+                        if (x >= total) continue;
+                        const int br = br0 + x / PER_BR, rem = x % PER_BR;
+                        const int jg = rem / (WGN * 64), wl = rem % (WGN * 64);
+                        const int ln = wl % 64, j = jg / GPA, g = jg % GPA;
+                        // the accumulator layout of the K-loop kernel (see the
+                        // epilogue below)
+                        const int row = br * MF + (ln % MF);
+                        const int col = (wl / 64) * WN + j * MF +
+                                        ((MF == 32) ? 8 * g + 4 * (ln >> 5) : 4 * (ln >> 4));
+                        uint2 w;
+                        w.x = cvt_pack<BF16>(sum[c][0], sum[c][1]);
+                        w.y = cvt_pack<BF16>(sum[c][2], sum[c][3]);
+                        const int chunk = col >> 3, half = (col >> 2) & 1;
+                        *reinterpret_cast<uint2*>(Cs + row * CROW + ((chunk ^ (row & 7)) << 4) +
+                                                  (half << 3)) = w;
+                    }
                 }
-                s_ok = ok;
-            }
-            __syncthreads();
-            if (!s_ok) continue;
-            // 3. the sum in slice order over the covered blocks
-            if constexpr (!kBig) {
-                // Small accumulators fold in registers:
-                // tmp = p0 + ... + p(ks-1), acc = tmp + acc, which is
-                // (p0 + ... + p(ks-1)) + p(ks) since addition commutes, then
-                // acc += p(ks+1), ... in slice order.
-                acc_t tmp[MI][NI];
-                for (int q = 0; q < ks; ++q) add_partial(tmp, q, q == 0);
-                if (ks > 0) {
-#pragma unroll
-                    for (int i = 0; i < MI; ++i)
-#pragma unroll
-                        for (int j = 0; j < NI; ++j)
-#pragma unroll
-                            for (int e = 0; e < ACC_N; ++e)
-                                if (covered(i, true)) acc[i][j][e] = tmp[i][j][e] + acc[i][j][e];
-                }
-                for (int q = ks + 1; q < p.split; ++q) add_partial(acc, q, false);
             } else {
-                // Two slices: acc + the other partial, which is p0 + p1 either
-                // way (fp32 addition commutes).  More: this slice's partial
-                // joined the others in memory and the sum is formed
-                // p0 + p1 + ... in slice order.  (One call site of
-                // add_partial: with two, the compiler spills inside the K
-                // loop.)
-                const int nq = p.split == 2 ? 1 : p.split;
-                for (int n = 0; n < nq; ++n)
-                    add_partial(acc, p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
+                // 1. partials: every slice but the last-arriving one (banded:
+                // every slice, for the other bands' rows), and the reducing
+                // slice's own rows when it sums from memory
+                // (the first kernel of the reduction-kernel mode, which takes
+                // no ticket and so is never last, writes its whole partial and
+                // moves on: the second kernel sums them; one call site of
+                // put_partial, as two spill inside the K loop)
+                if (!last || own_to_memory) put_partial(ks);
+                if (p.sk_band == 2) continue;
+                if (!last) {
+                    symtile::wg_stores_done();
+                    // (partials are always stored write-through)
+                    if (tid == 0) symtile::flag_publish_written_through(cnt + 1);
+                    if (!banded) continue;
+                } else if (own_to_memory) {
+                    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+                }
+                // 2. wait for the others' partials (bounded); they were written
+                // through and are read with coherent loads, so the wait needs
+                // no L2 invalidate
+                if (tid == 0) {
+                    const uint32_t target = banded ? (uint32_t)p.split : (uint32_t)p.split - 1;
+                    const bool ok = symtile::flag_wait_coherent(cnt + 1, target, p.spin_limit);
+                    if (ok && !banded) {
+                        // every slice of this call has counted itself: the next
+                        // call starts again from zero (banded: reset by the last
+                        // slice to store its band, below)
+                        symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
+                        symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                    } else if (!ok) {
+                        // a slice that holds a ticket may still count itself
+                        // later, so the counters are left as they are: the next
+                        // call that uses this workspace then draws tickets past
+                        // the slice count and reports ERR_WORKSPACE instead of
+                        // summing stale partials, until the caller zeroes them
+                        symtile::raise_error(p.err, symtile::ERR_TIMEOUT);
+                    }
+                    s_ok = ok;
+                }
+                __syncthreads();
+                if (!s_ok) continue;
+                // 3. the sum in slice order over the covered blocks
+                if constexpr (!kBig) {
+                    // Small accumulators fold in registers:
+                    // tmp = p0 + ... + p(ks-1), acc = tmp + acc, which is
+                    // (p0 + ... + p(ks-1)) + p(ks) since addition commutes, then
+                    // acc += p(ks+1), ... in slice order.
+                    acc_t tmp[MI][NI];
+                    for (int q = 0; q < ks; ++q) add_partial(tmp, q, q == 0);
+                    if (ks > 0) {
+    #pragma unroll
+                        for (int i = 0; i < MI; ++i)
+    #pragma unroll
+                            for (int j = 0; j < NI; ++j)
+    #pragma unroll
+                                for (int e = 0; e < ACC_N; ++e)
+                                    if (covered(i, true)) acc[i][j][e] = tmp[i][j][e] + acc[i][j][e];
+                    }
+                    for (int q = ks + 1; q < p.split; ++q) add_partial(acc, q, false);
+                } else {
+                    // Two slices: acc + the other partial, which is p0 + p1 either
+                    // way (fp32 addition commutes).  More: this slice's partial
+                    // joined the others in memory and the sum is formed
+                    // p0 + p1 + ... in slice order.  (One call site of
+                    // add_partial: with two, the compiler spills inside the K
+                    // loop.)
+                    const int nq = p.split == 2 ? 1 : p.split;
+                    for (int n = 0; n < nq; ++n)
+                        add_partial(acc, p.split == 2 ? 1 - ks : n, p.split != 2 && n == 0);
+                }
             }
         }
 
         // ---- epilogue: round, restage row-major, store, release --------
         // (banded split-K: only this slice's band is restaged and stored)
+        // (the reduction kernel staged its band above)
         uint8_t* Cs = smem;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
-            if (banded && block_band(i) != ks) continue;
+            if (RED || (banded && block_band(i) != ks)) continue;
 #pragma unroll
             for (int j = 0; j < NI; ++j)
 #pragma unroll
@@ -988,8 +1085,10 @@ void gas_kernel(const GasParams p) {
 
         // FUSED: every slot.  WAVE_SPEC: the local slot (the copy wave does the
         // rest during the next tile), except for this workgroup's last tile.
-        const int n_dst =
-            (p.role == ROLE_FUSED || (CW && t + G >= p.num_tiles)) ? p.world : 1;
+        const int n_dst = (p.role == ROLE_FUSED || (reducer && p.reduce_all) ||
+                           (CW && t + G >= p.num_tiles))
+                              ? p.world
+                              : 1;
         const uint16_t* tile_local = out_tile_ptr(p, BM, BN, tm, tn);
         const symtile::TileGeom geom = out_tile<BM, BN, THREADS>(p, tm, tn);
         const symtile::TileLanes lanes = symtile::tile_lanes(geom, tid, THREADS);
@@ -1024,7 +1123,33 @@ void gas_kernel(const GasParams p) {
         symtile::wg_stores_done();     // also orders the LDS reads above before reuse
         if (tid < 64) {                // wave 0: one release, then lane d counts slot rank + d
             bool publish = true;
-            if (banded) {
+            if (reducer) {
+                // Reduction kernel: the tile is whole once every band is
+                // stored; each band releases its stores and takes a ticket,
+                // and the one that draws the last resets the counter and
+                // publishes the tile's counters.  This mode leaves counter 1
+                // alone, so a non-zero counter 1 (or a ticket past the band
+                // count) means the workspace was not zero when the call
+                // started: the data stored is this call's, but the tile is
+                // not published, and the error is reported.
+                release_output(p.nontemporal);
+                uint32_t* cnt = p.sk_cnt + 2 * (tm * p.tiles_n + tn);
+                uint32_t u = 0, w1 = 0;
+                if (tid == 0) {
+                    u = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
+                    w1 = symtile::atomic_or<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
+                    if (w1 != 0 || u >= (uint32_t)p.reduce_bands)
+                        symtile::raise_error(p.err, symtile::ERR_WORKSPACE);
+                }
+                u = __shfl(u, 0);
+                w1 = __shfl(w1, 0);
+                publish = w1 == 0 && u == (uint32_t)p.reduce_bands - 1u;
+                if (publish) {
+                    if (p.nontemporal != 2) symtile::fence_acquire<__HIP_MEMORY_SCOPE_AGENT>();
+                    if (tid == 0)
+                        symtile::atomic_xchg<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 0u);
+                }
+            } else if (banded) {
                 // Banded: the tile is whole once every slice has stored its
                 // band.  Each slice releases its stores and takes a second
                 // ticket on counter 0 (the first round of tickets left it at
@@ -1100,6 +1225,7 @@ struct Variant {
     const void* consumer;
     int copy_threads;            // workgroup size of scatter_kernel and consumer_kernel
     const void* gas_ws;          // wave-specialised kernel (NW compute waves + 1), or null
+    const void* reduce;          // second kernel of the split-K reduction-kernel mode
     int band_q;                  // banded split-K: a band's rows must be a multiple of this
 };
 
@@ -1127,6 +1253,7 @@ Variant make_variant() {
                    reinterpret_cast<const void*>(&scatter_kernel<BM, BN>),
                    reinterpret_cast<const void*>(&consumer_kernel<BM, BN>),
                    copy_threads<BM>(), wave_spec_kernel<BM, BN, BF16, NW, MF, WS>(),
+                   reinterpret_cast<const void*>(&gas_kernel<BM, BN, BF16, NW, MF, false, true>),
                    band_quantum<BM, BN, NW, MF>()};
 }
 
@@ -1268,8 +1395,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     if (cfg.waves_per_wg != 0 && cfg.waves_per_wg != 4 && cfg.waves_per_wg != 8)
         return fail(SYMTILE_EINVAL, "waves_per_wg must be 0, 4 or 8");
     if (cfg.split_k < 0 || cfg.split_k > kMaxSplit) return fail(SYMTILE_EINVAL, "split_k must be 0..64");
-    if (cfg.split_reduce < SYMTILE_SPLIT_REDUCE_AUTO || cfg.split_reduce > SYMTILE_SPLIT_REDUCE_BANDED)
-        return fail(SYMTILE_EINVAL, "split_reduce must be 0, 1 or 2");
+    if (cfg.split_reduce < SYMTILE_SPLIT_REDUCE_AUTO || cfg.split_reduce > SYMTILE_SPLIT_REDUCE_KERNEL)
+        return fail(SYMTILE_EINVAL, "split_reduce must be 0, 1, 2 or 3");
     const int split = cfg.split_k > 1 ? cfg.split_k : 1;
     if (split > 1 && cfg.variant != SYMTILE_FUSED_SEQ && cfg.variant != SYMTILE_BULK_SYNC)
         return fail(SYMTILE_EUNSUPPORTED, "split_k > 1 is built for BULK_SYNC and FUSED_SEQ");
@@ -1380,6 +1507,8 @@ extern "C" symtile_status symtile_gemm_all_scatter(
 
     const int ntiles = (int)num_tiles;
     p.sk_band = 0;
+    p.reduce_bands = 1;
+    p.reduce_all = 0;
     if (cfg.variant == SYMTILE_FUSED_SEQ || cfg.variant == SYMTILE_BULK_SYNC) {
         int g = cfg.gemm_wgs > 0 ? cfg.gemm_wgs : std::min(p.units, cus);
         g = std::min(g, p.units);
@@ -1396,16 +1525,41 @@ extern "C" symtile_status symtile_gemm_all_scatter(
                             "(tiles * split_k <= " + std::to_string(limit) +
                                 ") and tile_m / split_k a multiple of " +
                                 std::to_string(v->band_q));
-            // AUTO: banded for two slices, where each slice reduces half the
-            // tile and the round trips match the last-arriver's; with more
-            // slices every slice's partial write, wait and second ticket
-            // cost more than the shared stores save
+            // AUTO: for two slices banded where it fits (each slice reduces
+            // half the tile, with the last-arriver's round trips), else the
+            // last arriver, both ahead of a second kernel; with more slices
+            // the reduction kernel, which spreads the sum and the stores over
+            // every CU instead of one slice per tile (banded: every slice
+            // then pays a partial write, a wait and a second ticket)
+            const bool automatic = cfg.split_reduce == SYMTILE_SPLIT_REDUCE_AUTO;
             p.sk_band = cfg.split_reduce == SYMTILE_SPLIT_REDUCE_BANDED ||
-                        (cfg.split_reduce == SYMTILE_SPLIT_REDUCE_AUTO && fits && split == 2);
+                        (automatic && fits && split == 2);
+            if (cfg.split_reduce == SYMTILE_SPLIT_REDUCE_KERNEL || (automatic && split > 2))
+                p.sk_band = 2;
         }
         p.role = cfg.variant == SYMTILE_FUSED_SEQ ? ROLE_FUSED : ROLE_LOCAL_ONLY;
         void* args[] = {&p};
         SYMTILE_HIP(hipLaunchKernel(v->gas, dim3(g), dim3(64 * v->waves), args, 0, stream));
+        if (p.sk_band == 2) {
+            // Reduction kernel: every (tile, band of rows) sums its rows of
+            // the partials in slice order and stores them.  Bands: the most
+            // (a power of two, whole accumulator blocks and store passes)
+            // that keep the grid within the CU count.
+            GasParams r = p;
+            int nb = 1;
+            while (cfg.tile_m % (2 * nb) == 0 && (cfg.tile_m / (2 * nb)) % v->band_q == 0 &&
+                   (size_t)ntiles * 2 * nb <= (size_t)cus)
+                nb *= 2;
+            r.role = ROLE_REDUCE;
+            r.sk_band = 0;
+            r.reduce_bands = nb;
+            r.reduce_all = cfg.variant == SYMTILE_FUSED_SEQ;
+            r.units = ntiles * nb;
+            r.gemm_wgs = std::min(r.units, cus);
+            void* rargs[] = {&r};
+            SYMTILE_HIP(hipLaunchKernel(v->reduce, dim3(r.gemm_wgs), dim3(64 * v->waves), rargs, 0,
+                                        stream));
+        }
         if (cfg.variant == SYMTILE_BULK_SYNC && world_size > 1) {
             int c = cfg.copy_wgs > 0 ? cfg.copy_wgs : cus;
             c = std::min(c, ntiles);

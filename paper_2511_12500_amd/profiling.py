@@ -3,6 +3,9 @@
 Turns a ``--kernel-trace --stats`` kernel_stats CSV and two ``--pmc`` runs
 (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch) into a short text summary:
 average launch duration of one kernel, and its memory traffic per launch.
+Calls made of several kernels (the split-K reduction kernel follows the
+K-loop kernel) name the others with ``--also``: each gets its own lines, and
+``call_avg_ns`` / ``bytes_per_call`` sum the kernels of one call.
 An optional third ``--pmc`` run (GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES,
 SQ_BUSY_CU_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 or _F16) adds the clock the
 kernel ran at, the share of SIMD cycles its matrix cores were busy, and its
@@ -171,6 +174,8 @@ def main(argv=None) -> int:
     ap.add_argument("--fetch")
     ap.add_argument("--write")
     ap.add_argument("--kernel", required=True, help="regex of the kernel to summarise")
+    ap.add_argument("--also", action="append", default=[],
+                    help="regex of another kernel of the same call (repeatable)")
     ap.add_argument("--calib", default="direct_copy", help="regex of the calibration copy")
     ap.add_argument("--calib-bytes", type=float, default=float(1 << 28),
                     help="bytes the calibration copy reads (and writes)")
@@ -196,6 +201,14 @@ def main(argv=None) -> int:
               f"- avg_ns: {t['avg_ns']:.0f}",
               f"- min_ns: {t['min_ns']:.0f}",
               f"- max_ns: {t['max_ns']:.0f}"]
+    others = [trace_last(a.trace, k, a.last) if a.last else trace_stats(a.trace, k)
+              for k in a.also]
+    for o in others:
+        lines += ["", f"- also kernel: `{o['name']}`", f"- also calls: {o['calls']}",
+                  f"- also avg_ns: {o['avg_ns']:.0f}"]
+    if others:
+        lines += [f"- call_avg_ns: {t['avg_ns'] + sum(o['avg_ns'] for o in others):.0f} "
+                  f"(the {1 + len(others)} kernels of one call)"]
     if a.fetch and a.write:
         fk, n_f, _ = counter_per_dispatch(a.fetch, "FETCH_SIZE", a.kernel)
         wk, n_w, _ = counter_per_dispatch(a.write, "WRITE_SIZE", a.kernel)
@@ -213,9 +226,20 @@ def main(argv=None) -> int:
                   f"- write_bytes_per_dispatch: {write_b:.0f}",
                   f"- bytes_per_dispatch: {fetch_b + write_b:.0f}",
                   f"- counted bytes / avg duration: {(fetch_b + write_b) / t['avg_ns']:.1f} GB/s"]
+        call_b = fetch_b + write_b
+        for k in a.also:
+            ofk, _, _ = counter_per_dispatch(a.fetch, "FETCH_SIZE", k)
+            owk, _, _ = counter_per_dispatch(a.write, "WRITE_SIZE", k)
+            ob = ofk * f_scale + owk * w_scale
+            call_b += ob
+            lines.append(f"- also fetch / write bytes per dispatch: {ofk * f_scale:.0f} / "
+                         f"{owk * w_scale:.0f}")
+        if a.also:
+            lines.append(f"- bytes_per_call: {call_b:.0f}")
         if a.algorithmic_bytes:
             lines.append(f"- algorithmic_bytes_per_dispatch: {a.algorithmic_bytes:.0f} "
-                         f"(counters / algorithmic = {(fetch_b + write_b) / a.algorithmic_bytes:.2f})")
+                         f"(counters / algorithmic = {call_b / a.algorithmic_bytes:.2f}"
+                         + (", whole call)" if a.also else ")"))
     if a.mfma:
         lines += mfma_lines(a.mfma, a.kernel, a.last, a.cus, a.xcds, a.flops, a.peak_clock_ghz,
                             a.flops_per_clk_cu)

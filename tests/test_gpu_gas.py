@@ -417,15 +417,18 @@ def test_padded_strides_on_tightly_sized_buffers():
             check_gathered(p, {rank: oracle_block_bounded(p.A, p.shards[rank], "bf16")})
 
 
-@pytest.mark.parametrize("mode", [1, 2], ids=["last", "banded"])
-def test_split_k_timeout_then_stale_workspace_is_reported(mode):
+@pytest.mark.parametrize("mode,again", [(1, 1), (2, 2), (1, 3), (2, 3)],
+                         ids=["last", "banded", "last_then_kernel", "banded_then_kernel"])
+def test_split_k_timeout_then_stale_workspace_is_reported(mode, again):
     """A slice allowed one poll gives up on the tiles whose partner partial
     is not yet counted (ETIMEOUT at the barrier) and leaves their counters as
     they are (last-arriver reduction: the two tickets; banded: the two first
     tickets plus the second ticket of a slice that went on).  A later call on
     the same workspace, made without zeroing it, reports the stale counters
-    (EINVAL at the barrier) and writes no stale sum; the Python wrapper
-    zeroes the workspace after either report, and its next call is exact."""
+    (EINVAL at the barrier): the ticketed reductions write no stale sum; the
+    reduction kernel (whose partials are all this call's) stores the tiles
+    but publishes none of the stale ones.  The Python wrapper zeroes the
+    workspace after either report, and its next call is exact."""
     pkg = sym()
     world, rank = 2, 0
     p = Problem(world, 1024, 512, 2048, "bf16", 64, 64, seed=17)     # 128 tiles x 2 slices
@@ -450,22 +453,31 @@ def test_split_k_timeout_then_stale_workspace_is_reported(mode):
         # the same workspace again, through the C ABI (no reset)
         ws = p.out.ws
         p.out.C_all().view(torch.int16).fill_(-1)
+        flags0 = p.out.arrived_all().cpu().numpy().copy()
         pkg.symtile_gemm_all_scatter(
             p.heap.handle, p.dA.data_ptr(), p.dB[rank].data_ptr(), p.heap.ptr(rank, p.out.c_off),
             p.heap.ptr(rank, p.out.flag_off), p.out.ready.data_ptr(), p.M, p.N, p.K, p.K, p.N,
             pkg.BF16, rank, world,
             pkg.GasConfig(variant=FUSED, tile_m=64, tile_n=64, split_k=2,
                           workspace=ws.data_ptr(), workspace_bytes=ws.numel(),
-                          split_reduce=mode),
+                          split_reduce=again),
             pkg.current_stream())
         with pytest.raises(pkg.SymtileError) as e:
             p.heap.barrier()
         assert e.value.name == "EINVAL" and "workspace" in str(e.value)
         torch.cuda.synchronize()
         G = u16(p.out.C_all())[0][:, :p.N].reshape(16, 64, 8, 64)
-        tm, tn = np.nonzero(stale[:, 0].reshape(16, 8))
-        for m, n in zip(tm, tn):             # a stale tile is left unwritten
-            assert np.all(G[m, :, n, :] == SENTINEL), (m, n)
+        bad = (stale != 0).any(axis=1).reshape(16, 8)
+        tm, tn = np.nonzero(bad)
+        if again != 3:
+            for m, n in zip(tm, tn):         # a stale tile is left unwritten
+                assert np.all(G[m, :, n, :] == SENTINEL), (m, n)
+        else:
+            # every tile stored, exact; the stale ones unpublished in every slot
+            check_block(G.reshape(p.M, p.N), want[rank], "bf16")
+            d = p.out.arrived_all().cpu().numpy() - flags0      # [slot, rank, tm, tn]
+            assert np.all(d[:, rank][:, bad] == 0)
+            assert np.all(d[:, rank][:, ~bad] == 1)
     # the wrapper zeroes the workspace after a failed barrier: exact again
     p.sentinel()
     p.calls[:] = 0
@@ -699,6 +711,34 @@ def test_banded_split_reduce_matches_last_arriver_bitwise(case):
         heaps[mode] = got
 
 
+@pytest.mark.parametrize("case", SPLITK + BANDED[1:3],
+                         ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_s%d" % c)
+@pytest.mark.parametrize("variant", [FUSED, BULK], ids=VNAMES.get)
+def test_reduction_kernel_matches_last_arriver_bitwise(case, variant):
+    """The reduction-kernel mode (every slice writes its partial, a second
+    kernel sums each tile's bands in slice order and stores them) gives the
+    last-arriver reduction's bits, at the default grid and at grids of 7 and
+    1 workgroups for the first kernel; against the oracle with the
+    accumulation bound, counters exact, workspace counters back at zero."""
+    pkg = sym()
+    world, M, N, K, tm, tn, dtype, split = case
+    rank = world // 2
+    p = Problem(world, M, N, K, dtype, tm, tn, seed=23)
+    want = {rank: oracle_block_bounded(p.A, p.shards[rank], dtype)}
+    ref = None
+    for mode, g in ((pkg.SPLIT_REDUCE_LAST, 0), (pkg.SPLIT_REDUCE_KERNEL, 0),
+                    (pkg.SPLIT_REDUCE_KERNEL, 7), (pkg.SPLIT_REDUCE_KERNEL, 1)):
+        p.sentinel()
+        p.run(rank, variant, split_k=split, split_reduce=mode, gemm_wgs=g)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[rank]))
+        assert np.all(_ws_counters(p) == 0), (mode, g)
+        got = u16(p.out.C_all())
+        if ref is None:
+            ref = got
+        assert np.array_equal(got, ref), (mode, g)
+
+
 def test_banded_split_reduce_argument_errors():
     """BANDED needs one resident workgroup per slice and whole bands;
     otherwise EUNSUPPORTED (AUTO falls back to the last-arriver reduction)."""
@@ -708,7 +748,7 @@ def test_banded_split_reduce_argument_errors():
         with pytest.raises(pkg.SymtileError, match="EUNSUPPORTED"):
             p.out.run(p.dA, p.dB[0], 0, FUSED, split_reduce=pkg.SPLIT_REDUCE_BANDED, **kw)
     with pytest.raises(pkg.SymtileError, match="EINVAL"):
-        p.out.run(p.dA, p.dB[0], 0, FUSED, split_k=2, split_reduce=3)
+        p.out.run(p.dA, p.dB[0], 0, FUSED, split_k=2, split_reduce=4)
     want = {0: oracle_block(p.A, p.shards[0], "bf16")}
     p.sentinel()
     p.run(0, FUSED, split_k=3)                     # AUTO: 128 rows do not split in 3 bands

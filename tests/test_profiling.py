@@ -55,6 +55,35 @@ def test_last_n_dispatches_and_calibrated_bytes(csvs, tmp_path):
     assert f"- source_sha: {profiling.sources_sha([str(src)])}" in text
 
 
+def test_call_of_two_kernels_sums_durations_and_bytes(csvs, tmp_path):
+    """--also adds a second kernel of the same call: its own lines, and the
+    call's duration and bytes are the sums."""
+    r = "void gas_kernel<256, 256, true, 8, true>(P)"
+    _write(csvs / "trace2.csv", ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+           [["void gas_kernel<256, 256, true, 8, false>(P)", 1000, 1400], [r, 1450, 1500],
+            ["void gas_kernel<256, 256, true, 8, false>(P)", 2000, 2200], [r, 2250, 2330]])
+    hdr = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    _write(csvs / "fetch2.csv", hdr,
+           [[1, "void gas_kernel<256, 256, true, 8, false>(P)", "FETCH_SIZE", 100],
+            [2, r, "FETCH_SIZE", 30], [4, "elementwise_kernel_manual_unroll<...>", "FETCH_SIZE", 64]])
+    _write(csvs / "write2.csv", hdr,
+           [[1, "void gas_kernel<256, 256, true, 8, false>(P)", "WRITE_SIZE", 10],
+            [2, r, "WRITE_SIZE", 20], [5, "elementwise_kernel_manual_unroll<...>", "WRITE_SIZE", 128]])
+    out = tmp_path / "call.md"
+    profiling.main(["--trace", str(csvs / "trace2.csv"), "--last", "2",
+                    "--kernel", r"gas_kernel<256, 256, true, 8, false>",
+                    "--also", r"gas_kernel<256, 256, true, 8, true>",
+                    "--fetch", str(csvs / "fetch2.csv"), "--write", str(csvs / "write2.csv"),
+                    "--calib", "elementwise", "--calib-bytes", "128", "--out", str(out)])
+    text = out.read_text()
+    assert "- avg_ns: 300" in text                      # (400 + 200) / 2
+    assert "- also avg_ns: 65" in text                  # (50 + 80) / 2
+    assert "- call_avg_ns: 365" in text
+    assert "- bytes_per_dispatch: 210" in text          # 100 x 2 + 10 x 1
+    assert "- also fetch / write bytes per dispatch: 60 / 20" in text
+    assert "- bytes_per_call: 290" in text
+
+
 def test_kernel_stats_without_counters(csvs, tmp_path):
     out = tmp_path / "s.md"
     profiling.main(["--trace", str(csvs / "stats.csv"), "--kernel", "gas_kernel",
@@ -75,6 +104,11 @@ def test_bench_reads_traffic_only_for_matching_sources(tmp_path, monkeypatch):
     src.write_text("v2")                               # kernel changed since the counters
     assert bench.counter_traffic("gas.md", [str(src)]) is None
     assert bench.counter_traffic("absent.md", [str(src)]) is None
+    # a call of several kernels: the whole call's bytes
+    src.write_text("v1")
+    prof.write_text(f"- bytes_per_dispatch: 1234\n- bytes_per_call: 2000\n"
+                    f"- source_sha: {bench.sources_sha([str(src)])}\n")
+    assert bench.counter_traffic("gas.md", [str(src)]) == 2000.0
 
 
 def test_source_hash_ignores_comments_and_layout(tmp_path):
