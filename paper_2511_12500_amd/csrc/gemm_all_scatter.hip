@@ -827,6 +827,9 @@ void gas_kernel(const GasParams p) {
         const int band_rows = banded ? BM / (reducer ? p.reduce_bands : p.split) : BM;
         // band of accumulator block row i of this wave (blocks are MF rows)
         auto block_band = [&](int i) { return (wm * WM + i * MF) / band_rows; };
+        // reduction kernel: counter 1 of the tile as the band found it (read
+        // before the sums, so its round trip overlaps them)
+        [[maybe_unused]] uint32_t red_cnt1 = 0;
         if (!CW && p.split > 1) {
             __shared__ uint32_t s_ticket, s_ok;
             const int tile = tm * p.tiles_n + tn;
@@ -929,6 +932,9 @@ void gas_kernel(const GasParams p) {
                 constexpr int CH = 4, QB = 4;
                 const int total = band_rows / MF * PER_BR;
                 const int br0 = ks * (band_rows / MF);
+                if (tid == 0)
+                    red_cnt1 = __hip_atomic_load(symtile::global_ptr(cnt + 1), __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
                 uint8_t* Cs = smem;
 #pragma unroll 1
                 for (int x0 = 0; x0 < total; x0 += THREADS * CH) {
@@ -1128,21 +1134,20 @@ void gas_kernel(const GasParams p) {
                 // stored; each band releases its stores and takes a ticket,
                 // and the one that draws the last resets the counter and
                 // publishes the tile's counters.  This mode leaves counter 1
-                // alone, so a non-zero counter 1 (or a ticket past the band
-                // count) means the workspace was not zero when the call
-                // started: the data stored is this call's, but the tile is
-                // not published, and the error is reported.
+                // alone, so a non-zero counter 1 (read above) or a ticket
+                // past the band count means the workspace was not zero when
+                // the call started: the data stored is this call's, but the
+                // tile is not published, and the error is reported.
                 release_output(p.nontemporal);
                 uint32_t* cnt = p.sk_cnt + 2 * (tm * p.tiles_n + tn);
-                uint32_t u = 0, w1 = 0;
+                uint32_t u = 0;
                 if (tid == 0) {
                     u = symtile::atomic_add<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt, 1u);
-                    w1 = symtile::atomic_or<__ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT>(cnt + 1, 0u);
-                    if (w1 != 0 || u >= (uint32_t)p.reduce_bands)
+                    if (red_cnt1 != 0 || u >= (uint32_t)p.reduce_bands)
                         symtile::raise_error(p.err, symtile::ERR_WORKSPACE);
                 }
                 u = __shfl(u, 0);
-                w1 = __shfl(w1, 0);
+                const uint32_t w1 = __shfl(red_cnt1, 0);
                 publish = w1 == 0 && u == (uint32_t)p.reduce_bands - 1u;
                 if (publish) {
                     if (p.nontemporal != 2) symtile::fence_acquire<__HIP_MEMORY_SCOPE_AGENT>();
