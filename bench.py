@@ -28,6 +28,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import statistics
 import sys
@@ -111,6 +112,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-sweep", action="store_true",
                     help="only the headline legs (no configs array, no per-config oracle)")
     ap.add_argument("--sweep-steps", type=int, default=20, help="timed launches per configs entry")
+    ap.add_argument("--sweep-min-ms", type=float, default=2.0,
+                    help="configs entries time at least this long (more launches for short calls)")
     ap.add_argument("--workload", default="gas_bf16_w8_m4096_k8192_n3584")
     ap.add_argument("--variant", default="fused_seq",
                     choices=["bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec"])
@@ -238,8 +241,11 @@ def per_call_median_ms(launch, torch, n: int) -> float:
 
 
 def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps, warmup,
-            label_args, with_median=False, split_reduce=0) -> dict:
-    """One timed GEMM + All-Scatter configuration on `case`."""
+            label_args, with_median=False, split_reduce=0, min_ms=0.0) -> dict:
+    """One timed GEMM + All-Scatter configuration on `case`.  With min_ms > 0
+    the number of timed launches is raised until they take about min_ms (from
+    the settling phase's pace), so that the gap before the first launch of a
+    short call weighs little."""
     wl = case.wl
     v = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
          "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[variant]
@@ -250,6 +256,8 @@ def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps,
         case.out.run(case.dA, case.dB, 0, v, **kw)
 
     st = settle(launch, torch, args)
+    if min_ms > 0 and st["launches"]:
+        steps = max(steps, math.ceil(min_ms / (st["ms"] / st["launches"])))
     # the per-call median of the measurement convention (one event pair per
     # call), before the timed region so that its launches are the last ones
     med = per_call_median_ms(launch, torch, 20) if with_median else None
@@ -263,7 +271,7 @@ def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps,
     peak = PEAK_MFMA_TFLOPS[wl.dtype]
     prof = gas_profile_name(label_args, wl)
     traffic = counter_traffic(prof, KERNEL_SOURCES)
-    return {"ms": ms, "tflops": tflops, "settle": st, "per_call_median_ms": med,
+    return {"ms": ms, "tflops": tflops, "settle": st, "per_call_median_ms": med, "steps": steps,
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": peak, "unit": "TFLOP/s",
                          "frac": tflops / peak, "traffic": traffic,
                          "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
@@ -329,13 +337,13 @@ def bench_sweep(args, torch, sym, workload) -> list:
         case = cases[key]
         label = _Label(args, variant, tile, split_k, g, c, red)
         r = gas_leg(args, torch, sym, case, variant, split_k, g, c, args.sweep_steps, 5, label,
-                    split_reduce=red)
+                    split_reduce=red, min_ms=args.sweep_min_ms)
         wl = case.wl
         out.append({"workload": name, "dtype": wl.dtype, "schedule": variant, "tile": tile,
                     "split_k": max(split_k, 1), "split_reduce": red, "gemm_wgs": g,
                     "copy_wgs": c,
                     "ms": r["ms"], "value": r["tflops"], "unit": "TFLOP/s",
-                    "steps": args.sweep_steps, "settle": r["settle"],
+                    "steps": r["steps"], "settle": r["settle"],
                     "roofline": r["roofline"]})
     for k in list(cases):
         cases.pop(k).close()
