@@ -347,6 +347,53 @@ def bench_sweep(args, torch, sym, workload) -> list:
                     "roofline": r["roofline"]})
     for k in list(cases):
         cases.pop(k).close()
+    out += graph_legs(args, torch, sym, workload)
+    return out
+
+
+# Workloads whose calls are short enough that the host's launch rate bounds
+# back-to-back calls: also timed as GRAPH_CALLS calls captured in one HIP
+# graph and replayed (workload, schedule, tile).
+GRAPH_CALLS = 20
+GRAPH_LEGS = [("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64")]
+
+
+def graph_legs(args, torch, sym, workload) -> list:
+    """Per-call time of GRAPH_CALLS calls replayed from one captured graph
+    (the launch overhead of the host leaves the timed region)."""
+    out = []
+    for name, variant, tile in GRAPH_LEGS:
+        wl = workload.GEMM_WORKLOADS[name]
+        case = GasCase(torch, sym, workload, wl, tile)
+        v = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ}[variant]
+        kw = dict(nontemporal=args.nontemporal, group_m=args.group_m)
+        case.out.run(case.dA, case.dB, 0, v, **kw)            # eager call before the capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(GRAPH_CALLS):
+                case.out.run(case.dA, case.dB, 0, v, **kw)
+        st = settle(g.replay, torch, args)
+        steps = max(args.sweep_steps, math.ceil(args.sweep_min_ms / (st["ms"] / st["launches"])))
+        for _ in range(5):
+            g.replay()
+        case.heap.barrier()
+        ms = time_back_to_back(g.replay, torch, steps) / (steps * GRAPH_CALLS)
+        case.heap.barrier()
+        tflops = wl.flops / (ms * 1e-3) / 1e12
+        peak = PEAK_MFMA_TFLOPS[wl.dtype]
+        out.append({"workload": name, "dtype": wl.dtype, "schedule": variant, "tile": tile,
+                    "split_k": 1, "split_reduce": 0, "gemm_wgs": 0, "copy_wgs": 0,
+                    "graph_calls": GRAPH_CALLS, "ms": ms, "value": tflops, "unit": "TFLOP/s",
+                    "steps": steps, "settle": st,
+                    "roofline": {"bound": "mfma", "achieved": tflops, "peak": peak,
+                                 "unit": "TFLOP/s", "frac": tflops / peak, "traffic": None,
+                                 "kernel": "gas_kernel<%d,%d,%s>" % (case.tm, case.tn, wl.dtype),
+                                 "algorithmic_flops_per_launch": wl.flops,
+                                 "algorithmic_bytes_per_launch": gemm_bytes(wl),
+                                 "avg_launch_ms": ms}})
+        del g
+        case.close()
     return out
 
 

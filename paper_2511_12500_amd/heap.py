@@ -185,7 +185,11 @@ class GatheredOutput:
         (BULK_SYNC, FUSED_SEQ): each tile is computed as that many K slices,
         with this object's workspace; calls on one object that use split-K
         must not overlap in time.  ``split_reduce``: SPLIT_REDUCE_AUTO (0),
-        SPLIT_REDUCE_LAST or SPLIT_REDUCE_BANDED (who sums the slices)."""
+        SPLIT_REDUCE_LAST, SPLIT_REDUCE_BANDED or SPLIT_REDUCE_KERNEL (who sums
+        the slices).  The call only launches kernels on the stream, so it can
+        be captured in a graph (torch.cuda.graph) and replayed, except WG_SPEC
+        and UNFUSED_PC, whose epoch is fixed at capture; make one eager split-K
+        call first so that the workspace exists before the capture."""
         if A.dtype != self.dtype or B_shard.dtype != self.dtype:
             raise TypeError("A and B_shard must have the output dtype")
         if not (A.is_cuda and B_shard.is_cuda and A.is_contiguous() and B_shard.is_contiguous()):

@@ -655,10 +655,12 @@ def test_split_k_all_ranks(case, variant):
 
 
 @pytest.mark.parametrize("split", [2, 3, 5])
-def test_split_k_is_deterministic_across_grids(split):
+@pytest.mark.parametrize("mode", [0, 1], ids=["auto", "last"])
+def test_split_k_is_deterministic_across_grids(split, mode):
     """The slices add their partials in slice order, so neither the grid size
-    (how many slices run at once, and which finishes last) nor a repeated
-    call changes a bit."""
+    (how many slices run at once, and which finishes last; down to one
+    workgroup for the last-slice reduction, which assumes no co-residency)
+    nor a repeated call changes a bit."""
     world, rank = 4, 2
     p = Problem(world, 520, 392, 1544, "bf16", 128, 128, seed=12)
     want = {rank: oracle_block(p.A, p.shards[rank], "bf16")}
@@ -666,7 +668,7 @@ def test_split_k_is_deterministic_across_grids(split):
     ref = None
     for g in (0, units, 7, 1, 0):
         p.sentinel()
-        p.run(rank, FUSED, split_k=split, gemm_wgs=g)
+        p.run(rank, FUSED, split_k=split, gemm_wgs=g, split_reduce=mode)
         p.barrier()
         check_gathered(p, want, flag_count=int(p.calls[rank]))
         got = u16(p.out.C_all())
@@ -795,16 +797,18 @@ def test_split_k_full_size_matches_oracle(wl, tile, split):
     assert np.all(_ws_counters(p) == 0)
 
 
-def test_split_k_trace_is_causal():
+@pytest.mark.parametrize("mode", [1, 3], ids=["last", "kernel"])
+def test_split_k_trace_is_causal(mode):
     """With split-K the start and main-loop words are slice 0's and the
-    stored and released words the reducing slice's; still in order."""
+    stored and released words the reducing slice's (or the last band of the
+    reduction kernel); still in order."""
     from paper_2511_12500_amd import trace as T
     world, rank = 4, 1
     p = Problem(world, 600, 520, 264, "bf16", 128, 128, seed=7)
     want = {rank: oracle_block(p.A, p.shards[rank], "bf16")}
     tr = p.out.new_trace()
     p.sentinel()
-    p.run(rank, FUSED, trace=tr, split_k=3)
+    p.run(rank, FUSED, trace=tr, split_k=3, split_reduce=mode)
     p.barrier()
     check_gathered(p, want)
     raw = tr.cpu().numpy().view(np.uint64)

@@ -32,21 +32,21 @@ def _noalloc(pkg, p, rank, variant, split_k, **kw):
     p.calls[rank] += 1
 
 
-CASES = [  # world, M, N, K, dtype, tile, split, rank, variant
-    (8, 1024, 1024, 4096, "bf16", (128, 128), 4, 0, FUSED),
-    (3, 300, 136, 520, "f16", (64, 64), 3, 2, BULK),
+CASES = [  # world, M, N, K, dtype, tile, split, rank, variant, split_reduce
+    (8, 1024, 1024, 4096, "bf16", (128, 128), 4, 0, FUSED, 0),     # reduction kernel
+    (3, 300, 136, 520, "f16", (64, 64), 3, 2, BULK, 1),            # last slice
 ]
 
 
 def test_noalloc_equals_the_workspace_call_on_two_calls_in_a_row():
     pkg = sym()
-    for world, M, N, K, dtype, (tm, tn), split, rank, variant in CASES:
+    for world, M, N, K, dtype, (tm, tn), split, rank, variant, red in CASES:
         ref = Problem(world, M, N, K, dtype, tm, tn, seed=M + K)
         got = Problem(world, M, N, K, dtype, tm, tn, seed=M + K)
         for p in (ref, got):
             p.sentinel()
-        ref.run(rank, variant, split_k=split)
-        _noalloc(pkg, got, rank, variant, split)
+        ref.run(rank, variant, split_k=split, split_reduce=red)
+        _noalloc(pkg, got, rank, variant, split, split_reduce=red)
         ref.barrier()
         got.barrier()
         want = {rank: oracle_block(got.A, got.shards[rank], dtype)}
