@@ -818,8 +818,13 @@ void gas_kernel(const GasParams p) {
         //    itself, waits until every slice has, and then sums band s in
         //    slice order and stores band s.  The reduction and the stores are
         //    shared by all slices instead of falling on the last one.
-        // Either way the sum is p0 + p1 + ... in slice order, so both give
-        // the same bits, whichever slice came last.  (Not built into the
+        //  * Reduction-kernel mode (p.sk_band == 2 here, then the RED
+        //    instantiation): every slice writes its whole partial and moves
+        //    on, taking no ticket; the second kernel sums each (tile, band of
+        //    rows) and stores it, and its bands take the tickets that decide
+        //    which one publishes the tile.
+        // Every way the sum is p0 + p1 + ... in slice order, so all give the
+        // same bits, whichever slice came last.  (Not built into the
         // copy-wave kernel: wave specialisation has no split-K, and its
         // third wave per SIMD leaves no registers for it.)
         const bool banded = !CW && p.split > 1 &&
