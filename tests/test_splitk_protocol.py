@@ -362,3 +362,129 @@ def test_banded_model_finds_the_planted_errors():
         _explore_banded(1, 2, R=2, wait_target=1)
     with pytest.raises(AssertionError, match="before every band|counters left|published"):
         _explore_banded(1, 2, R=2, publish_ticket=2)
+
+
+# ---------------------------------------------------------------------------
+# Reduction kernel.  The first kernel's slices write their whole partials and
+# take no ticket; the kernel boundary orders every partial before the second
+# kernel, whose work units are (tile t, band b) of NB bands, on a persistent
+# grid of G workgroups (workgroup g takes units g, g+G, ...):
+#
+#   c1 = written[t]                         (read before the sums; this mode
+#                                            never changes written[])
+#   sum band b of every partial ; store band b
+#   u = cnt[t]++                            (after a release)
+#   if c1 != 0 or u >= NB: report a stale workspace, publish nothing
+#   elif u == NB-1: acquire, cnt[t] = 0, publish the tile's counters
+#
+# Nothing waits, so any grid and any number of resident workgroups work.
+
+K_START, K_STORE, K_TICKET, K_PUBLISH, K_DONE = range(5)
+
+
+def _run_reduction_kernel(T, NB, G, R, cnt0, written0, check_c1=True):
+    """Every interleaving of the second kernel from counters cnt0/written0.
+    Returns the set of end states (cnt, written, published, flagged)."""
+    units = [[u for u in range(g, T * NB, G)] for g in range(G)]
+    full = (1 << NB) - 1
+    ends = set()
+    seen = set()
+
+    def explore(state):
+        if state in seen:
+            return
+        seen.add(state)
+        wgs, resident, cnt, stored, published, flagged = state
+        if all(i == len(units[g]) for g, (i, _, _) in enumerate(wgs)):
+            ends.add((cnt, tuple(written0), published, flagged))
+            return
+        moves = []
+        if len(resident) < R:
+            for g in range(G):
+                if g not in resident and wgs[g][0] == 0 and wgs[g][1] == K_START and units[g]:
+                    moves.append(("admit", g))
+        moves += [("step", g) for g in resident]
+        assert moves, f"deadlock in {state}"
+        for kind, g in moves:
+            w, res = list(wgs), list(resident)
+            c, st, pb, fl = list(cnt), list(stored), list(published), list(flagged)
+            if kind == "admit":
+                res.append(g)
+            else:
+                i, pc, c1 = w[g]
+                t, b = divmod(units[g][i], NB)
+                if pc == K_START:
+                    c1 = written0[t]
+                    pc = K_STORE
+                elif pc == K_STORE:
+                    st[t] |= 1 << b
+                    pc = K_TICKET
+                elif pc == K_TICKET:
+                    u = c[t]
+                    c[t] += 1
+                    stale = (check_c1 and c1 != 0) or u >= NB
+                    if stale:
+                        fl[t] += 1
+                        pc = K_DONE
+                    else:
+                        pc = K_PUBLISH if u == NB - 1 else K_DONE
+                elif pc == K_PUBLISH:
+                    assert st[t] == full, "tile published before every band was stored"
+                    c[t] = 0
+                    pb[t] += 1
+                    pc = K_DONE
+                if pc == K_DONE:
+                    i, pc, c1 = i + 1, K_START, 0
+                    if i == len(units[g]):
+                        res.remove(g)
+                w[g] = (i, pc, c1)
+            explore((tuple(w), tuple(res), tuple(c), tuple(st), tuple(pb), tuple(fl)))
+
+    explore((tuple((0, K_START, 0) for _ in range(G)), (), tuple(cnt0), (0,) * T, (0,) * T,
+             (0,) * T))
+    return ends
+
+
+@pytest.mark.parametrize("T,NB,G,R", [(1, 2, 2, 2), (1, 4, 4, 4), (1, 4, 1, 1), (2, 2, 3, 1),
+                                      (2, 3, 4, 2), (3, 2, 6, 6)])
+def test_reduction_kernel_publishes_each_tile_once_on_any_grid(T, NB, G, R):
+    """From clean counters: each tile published exactly once, only after all
+    its bands are stored, nothing reported, the ticket counter back at zero,
+    whatever the grid and however few workgroups are resident."""
+    zero = (0,) * T
+    for cnt, written, published, flagged in _run_reduction_kernel(T, NB, G, R, zero, zero):
+        assert cnt == zero and written == zero
+        assert published == (1,) * T and flagged == zero
+
+
+@pytest.mark.parametrize("T,S,G,R,NB", [(1, 2, 2, 2, 2), (1, 2, 2, 2, 4), (1, 3, 3, 2, 4),
+                                        (2, 2, 2, 2, 2)])
+def test_reduction_kernel_after_a_timeout_publishes_no_stale_tile(T, S, G, R, NB):
+    """Counters left by a timed-out last-slice call (every end state of the
+    timeout model): a tile whose ticket counter is non-zero always has a
+    non-zero written counter too, which is what the reduction kernel reads;
+    such a tile is reported by every band and never published, and its
+    counters stay non-zero, so later calls report it as well; clean tiles are
+    published once."""
+    zero = (0,) * T
+    first = _run_call(T, S, G, R, zero, zero, True, False, True)
+    assert any(any(tm) for *_, tm in first), "the model never timed out"
+    for cnt, written, *_ in first:
+        for t in range(T):
+            assert cnt[t] == 0 or written[t] != 0, (cnt, written)
+        for cnt2, written2, published, flagged in _run_reduction_kernel(T, NB, NB, NB, cnt,
+                                                                         written):
+            for t in range(T):
+                if cnt[t] == 0 and written[t] == 0:
+                    assert published[t] == 1 and flagged[t] == 0 and cnt2[t] == 0
+                else:
+                    assert published[t] == 0 and flagged[t] == NB, (published, flagged)
+                    assert cnt2[t] != 0 or written2[t] != 0
+
+
+def test_reduction_kernel_model_finds_the_planted_error():
+    """Pin: with the ticket check alone (no read of the written counter), a
+    tile left with S < NB tickets by a timed-out call is published after only
+    NB - S of its bands are stored."""
+    with pytest.raises(AssertionError, match="before every band"):
+        _run_reduction_kernel(1, 4, 4, 4, (2,), (1,), check_c1=False)
