@@ -371,7 +371,11 @@ def test_argument_errors():
     c0, f0 = p.heap.ptr(0, p.out.c_off), p.heap.ptr(0, p.out.flag_off)
     for bad in (dict(C=c_other, flags=f0), dict(C=c0, flags=f0, K=60),
                 dict(C=c0, flags=f0, rank=2), dict(C=c0, flags=f0, world=3),
-                dict(C=c0, flags=f0, M=100000)):
+                dict(C=c0, flags=f0, M=100000),
+                # maximum sizes: 32-bit buffer offsets; B of 2 GiB, a 64-row band of the
+                # gathered C of 2 GiB (rejected before any memory is touched)
+                dict(C=c0, flags=f0, K=1 << 20, N=1024),
+                dict(C=c0, flags=f0, N=1 << 23)):
         with pytest.raises(pkg.SymtileError) as e:
             call(**bad)
         assert e.value.name == "EINVAL", bad
