@@ -717,8 +717,9 @@ def test_banded_split_reduce_matches_last_arriver_bitwise(case):
         heaps[mode] = got
 
 
-@pytest.mark.parametrize("case", SPLITK + BANDED[1:3],
-                         ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_s%d" % c)
+@pytest.mark.parametrize("case", SPLITK + BANDED[1:3] + [
+    (2, 2048, 2048, 96, 64, 64, "f16", 3),     # 1024 tiles: reduction units past the CU count
+], ids=lambda c: "w%d_m%d_n%d_k%d_t%dx%d_%s_s%d" % c)
 @pytest.mark.parametrize("variant", [FUSED, BULK], ids=VNAMES.get)
 def test_reduction_kernel_matches_last_arriver_bitwise(case, variant):
     """The reduction-kernel mode (every slice writes its partial, a second
