@@ -323,6 +323,32 @@ def bench_gas(args, torch, sym, workload):
     return res, wl, A, B
 
 
+def library_baseline(args, torch, sym, workload) -> dict:
+    """The one-GPU analogue of the paper's baseline (torch.matmul followed by
+    an RCCL all-gather): torch.matmul of rank 0's share into a local tensor,
+    then torch copies of it into rank 0's block of every slot (no counters).
+    Timed like the headline leg, on the same workload; context, not a target."""
+    wl = workload.GEMM_WORKLOADS[args.workload]
+    case = GasCase(torch, sym, workload, wl, "256x256")
+    c_local = torch.empty(wl.M, wl.N_local, dtype=case.dA.dtype, device="cuda")
+    blocks = [case.out.C(s)[:, :wl.N_local] for s in range(wl.world)]
+
+    def launch():
+        torch.matmul(case.dA, case.dB, out=c_local)
+        for b in blocks:
+            b.copy_(c_local)
+
+    st = settle(launch, torch, args)
+    for _ in range(args.warmup):
+        launch()
+    ms = time_back_to_back(launch, torch, args.steps) / args.steps
+    del blocks
+    case.close()
+    return {"kind": "torch.matmul + torch copies of the block into the w slots",
+            "ms": ms, "value": wl.flops / (ms * 1e-3) / 1e12, "unit": "TFLOP/s",
+            "steps": args.steps, "settle": st}
+
+
 def bench_sweep(args, torch, sym, workload) -> list:
     """Every SWEEP entry, grouped so each workload and tile's buffers are
     built once."""
@@ -628,6 +654,7 @@ def main(argv=None):
     else:
         copy = None
     sweep = [] if args.no_sweep else bench_sweep(args, torch, sym, workload)
+    lib = None if args.no_sweep else library_baseline(args, torch, sym, workload)
     res, wl, A, B = bench_gas(args, torch, sym, workload)
     line = {
         "metric": METRIC,
@@ -653,6 +680,9 @@ def main(argv=None):
             line["tile_copy"]["cpu_baseline"] = copy_cpu_baseline(args, workload)
     if copies or sweep:
         line["configs"] = [dict(c, schedule="heap_copy") for c in copies] + sweep
+    if lib is not None:
+        lib["speedup_of_this_call"] = lib["ms"] / res["ms_per_step"]
+        line["library_baseline"] = lib
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args, wl, A, B, workload)
         if not args.no_sweep:
