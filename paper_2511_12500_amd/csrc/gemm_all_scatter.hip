@@ -41,9 +41,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <map>
 #include <mutex>
 #include <string>
 #include <type_traits>
+#include <utility>
 
 #include "symtile.h"
 #include "symtile_device.h"
@@ -1298,8 +1300,21 @@ const Variant* find_wave_spec_variant(int bm, int bn, bool bf16) {
 symtile_status coresident_limit(const Variant* v, int device, int* cus, int* limit) {
     int n_cu = symtile_host::cu_count(device);
     if (n_cu <= 0) return symtile_host::fail(SYMTILE_EHIP, "cannot read the CU count");
+    // workgroups of a kernel per CU: fixed for the process, so asked once per
+    // (kernel, device) (the query costs microseconds on every call's path)
+    static std::mutex mu;
+    static std::map<std::pair<const void*, int>, int> per_cu_known;
     int per_cu = 0;
-    SYMTILE_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->gas, 64 * v->waves, 0));
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = per_cu_known.find({v->gas, device});
+        if (it != per_cu_known.end()) per_cu = it->second;
+    }
+    if (per_cu == 0) {
+        SYMTILE_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->gas, 64 * v->waves, 0));
+        std::lock_guard<std::mutex> lock(mu);
+        per_cu_known[{v->gas, device}] = per_cu;
+    }
     *cus = n_cu;
     *limit = per_cu * n_cu;
     return SYMTILE_OK;
@@ -1685,7 +1700,7 @@ extern "C" symtile_status symtile_gemm_all_scatter_noalloc(
     hipLaunchKernelGGL(zero_words_kernel, dim3(std::min((words + 255) / 256, 1024)), dim3(256), 0,
                        static_cast<hipStream_t>(s), static_cast<uint32_t*>(scratch), words);
     const hipError_t e = hipGetLastError();
-    (void)hipSetDevice(prev);
+    if (prev >= 0) (void)hipSetDevice(prev);
     if (e != hipSuccess) return symtile_host::hip_fail(e, "zero_words_kernel launch");
     cfg.workspace = scratch;
     cfg.workspace_bytes = SYMTILE_NOALLOC_SCRATCH_BYTES;

@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -224,8 +225,10 @@ bool in_slot(const symtile_heap* h, const void* p, size_t bytes, int rank) {
 }
 
 symtile_status set_device(const symtile_heap* h, int* previous) {
-    if (previous) SYMTILE_HIP(hipGetDevice(previous));
-    SYMTILE_HIP(hipSetDevice(h->device));
+    int cur = -1;
+    SYMTILE_HIP(hipGetDevice(&cur));
+    if (previous) *previous = cur == h->device ? -1 : cur;
+    if (cur != h->device) SYMTILE_HIP(hipSetDevice(h->device));
     return SYMTILE_OK;
 }
 
@@ -238,9 +241,16 @@ symtile_status aux_stream(symtile_heap* h) {
 }
 
 int cu_count(int device) {
+    // a device's CU count does not change: read once per device
+    static std::atomic<int> known[64];
+    if (device >= 0 && device < 64) {
+        const int n = known[device].load(std::memory_order_relaxed);
+        if (n > 0) return n;
+    }
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
         return 0;
+    if (device >= 0 && device < 64) known[device].store(n, std::memory_order_relaxed);
     return n;
 }
 

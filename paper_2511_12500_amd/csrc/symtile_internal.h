@@ -50,7 +50,8 @@ symtile_status hip_fail(hipError_t e, const char* what);
 // True when [p, p + bytes) lies inside slot `rank` of h.
 bool in_slot(const symtile_heap* h, const void* p, size_t bytes, int rank);
 
-// Make h's device current for the calling thread; returns the previous one.
+// Make h's device current for the calling thread; *previous = the device to
+// restore afterwards, or -1 when h's device already was current.
 symtile_status set_device(const symtile_heap* h, int* previous);
 
 int cu_count(int device);

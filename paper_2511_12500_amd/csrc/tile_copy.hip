@@ -281,7 +281,7 @@ static symtile_status tile_copy_launch(symtile_heap* h, size_t src_off, size_t d
     hipError_t e = t0 ? hipExtLaunchKernel(kernel, grid, dim3(kThreads), args, 0, stream, t0, t1, 0)
                       : hipLaunchKernel(kernel, grid, dim3(kThreads), args, 0, stream);
     if (e == hipSuccess) e = hipGetLastError();
-    (void)hipSetDevice(prev);
+    if (prev >= 0) (void)hipSetDevice(prev);
     if (e != hipSuccess) return symtile_host::hip_fail(e, "tile_copy_kernel launch");
     return SYMTILE_OK;
 }

@@ -4,6 +4,8 @@ returns tensors living in the heap), and the symmetric buffers of one
 GEMM + All-Scatter problem.  Argument marshalling only."""
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
 from . import _binding as B
@@ -11,8 +13,18 @@ from . import _binding as B
 _SLOT_ALIGN = 2 << 20
 
 
-def current_stream() -> int:
-    return torch.cuda.current_stream().cuda_stream
+# The raw handle of the current stream, without building a torch Stream object
+# (which costs microseconds on every call's launch path); the public accessor
+# when this torch has no raw one.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def current_stream(device: int | None = None) -> int:
+    """The current torch stream of ``device`` (default: the current device)
+    as a raw stream handle."""
+    if _raw_stream is not None:
+        return _raw_stream(torch.cuda.current_device() if device is None else device)
+    return torch.cuda.current_stream(device).cuda_stream
 
 
 class Heap:
@@ -126,6 +138,14 @@ class GatheredOutput:
         self.ready_epoch = 0     # value of every ready counter after the last WG_SPEC call
         self.ws = None           # split-K workspace (uint8 device tensor), grown on demand
         self.ws_seen = heap.failed_barriers   # failed barriers already answered by a reset
+        # per-call constants, computed once (run() is on the host's launch path):
+        # the output's and counters' addresses per rank, the workspace size per
+        # slice count, and one config struct filled in by every call
+        self._ptrs = {}
+        self._ws_need = {}
+        self._cfg = B.GasConfig()
+        self._cfg_ref = ctypes.byref(self._cfg)
+        self._dt = B.BF16 if dtype == torch.bfloat16 else B.F16
 
     def C(self, rank: int) -> torch.Tensor:
         return self.heap.view(rank, self.c_off, (self.M, self.heap.world * self.N_local),
@@ -147,8 +167,10 @@ class GatheredOutput:
         """The split-K workspace for ``split_k`` slices (None when split_k <= 1):
         a zeroed uint8 device tensor, kept and reused by later calls (each call
         leaves its counters at zero), replaced by a larger one when needed."""
-        need = B.symtile_gas_workspace_bytes(self.M, self.N_local, self.tile_m, self.tile_n,
-                                             split_k)
+        need = self._ws_need.get(split_k)
+        if need is None:
+            need = self._ws_need[split_k] = B.symtile_gas_workspace_bytes(
+                self.M, self.N_local, self.tile_m, self.tile_n, split_k)
         if need == 0:
             return None
         if self.ws is None or self.ws.numel() < need:
@@ -204,18 +226,24 @@ class GatheredOutput:
                                   not trace.is_contiguous() or
                                   trace.numel() < self.tiles_m * self.tiles_n * B.TRACE_WORDS):
             raise ValueError("trace must be a contiguous int64 device tensor from new_trace()")
-        cfg = B.GasConfig(variant=variant, tile_m=self.tile_m, tile_n=self.tile_n,
-                          gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, epoch=max(self.ready_epoch, 1),
-                          spin_limit=spin_limit, nontemporal=nontemporal, group_m=group_m,
-                          waves_per_wg=waves_per_wg, copy_stream=copy_stream,
-                          trace=trace.data_ptr() if trace is not None else None)
-        cfg.split_k = split_k
-        cfg.split_reduce = split_reduce
+        ptrs = self._ptrs.get(rank)
+        if ptrs is None:
+            ptrs = self._ptrs[rank] = (self.heap.ptr(rank, self.c_off),
+                                       self.heap.ptr(rank, self.flag_off))
+        cfg = self._cfg
+        cfg.variant, cfg.tile_m, cfg.tile_n = variant, self.tile_m, self.tile_n
+        cfg.gemm_wgs, cfg.copy_wgs, cfg.epoch = gemm_wgs, copy_wgs, max(self.ready_epoch, 1)
+        cfg.spin_limit, cfg.nontemporal, cfg.group_m = spin_limit, nontemporal, group_m
+        cfg.waves_per_wg, cfg.copy_stream = waves_per_wg, copy_stream
+        cfg.trace = trace.data_ptr() if trace is not None else None
+        cfg.split_k, cfg.split_reduce = split_k, split_reduce
+        cfg.workspace, cfg.workspace_bytes = None, 0
         ws = self.workspace(split_k) if split_k > 1 else None
         if ws is not None:               # None: no tiles, nothing to keep
             cfg.workspace, cfg.workspace_bytes = ws.data_ptr(), ws.numel()
-        dt = B.BF16 if self.dtype == torch.bfloat16 else B.F16
-        B.symtile_gemm_all_scatter(
-            self.heap.handle, A.data_ptr(), B_shard.data_ptr(), self.heap.ptr(rank, self.c_off),
-            self.heap.ptr(rank, self.flag_off), self.ready.data_ptr(), M, N, K, K, N, dt, rank,
-            self.heap.world, cfg, current_stream() if stream is None else stream)
+        st = B.lib.symtile_gemm_all_scatter(
+            self.heap.handle, A.data_ptr(), B_shard.data_ptr(), ptrs[0], ptrs[1],
+            self.ready.data_ptr(), M, N, K, K, N, self._dt, rank, self.heap.world,
+            self._cfg_ref, current_stream(self.heap.device) if stream is None else stream)
+        if st:
+            B._check(st, "symtile_gemm_all_scatter")

@@ -80,3 +80,26 @@ def test_graph_replays_match_the_oracle_and_eager_calls(case):
         if split > 1:
             assert np.all(_ws_counters(p) == 0), rep
     del g
+
+
+def test_current_stream_is_torchs_current_stream():
+    """The binding launches on torch's current stream: the raw handle it
+    reads equals torch's, on the default stream, inside a stream context and
+    inside a graph capture (where the calls above are recorded)."""
+    from tests.gpu_util import sym
+    pkg = sym()
+    assert pkg.current_stream() == torch.cuda.current_stream().cuda_stream
+    assert pkg.current_stream(0) == torch.cuda.current_stream(0).cuda_stream
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        assert pkg.current_stream() == s.cuda_stream
+    g = torch.cuda.CUDAGraph()
+    seen = []
+    x = torch.zeros(4, device="cuda")
+    with torch.cuda.graph(g):
+        seen.append((pkg.current_stream(), torch.cuda.current_stream().cuda_stream))
+        x.add_(1)
+    assert seen[0][0] == seen[0][1]
+    g.replay()
+    torch.cuda.synchronize()
+    assert x.tolist() == [1.0] * 4
