@@ -120,6 +120,8 @@ def parse_args(argv=None):
     ap.add_argument("--tile", default=None,
                     help="output tile MxN (default 256x256; 256x128 for wave_spec, the only "
                          "tile that schedule is built for)")
+    ap.add_argument("--waves", type=int, default=0,
+                    help="waves per producer workgroup (0 = the tile's default)")
     ap.add_argument("--gemm-wgs", type=int, default=0)
     ap.add_argument("--copy-wgs", type=int, default=0)
     ap.add_argument("--group-m", type=int, default=0)
@@ -250,7 +252,8 @@ def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps,
     v = {"bulk_sync": sym.BULK_SYNC, "fused_seq": sym.FUSED_SEQ, "wg_spec": sym.WG_SPEC,
          "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[variant]
     kw = dict(gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, nontemporal=args.nontemporal,
-              group_m=args.group_m, split_k=split_k, split_reduce=split_reduce)
+              group_m=args.group_m, split_k=split_k, split_reduce=split_reduce,
+              waves_per_wg=getattr(args, "waves", 0))
 
     def launch():
         case.out.run(case.dA, case.dB, 0, v, **kw)

@@ -218,6 +218,20 @@ __device__ __forceinline__ f32x16_t mfma32(u32x4 a, u32x4 b, f32x16_t c) {
                                                       __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
 }
 
+// The 32x32x16 MFMA as an ordered statement: accumulating in place in
+// AGPRs, and a memory clobber, so the compiler keeps every memory access on
+// the side of it where the source puts it (the 4-wave loop lays out its own
+// interleaving of MFMAs, LDS accesses and loads this way).  The compiler
+// does not see the MFMA: its hazard wait states before the first use and
+// after the last are the caller's.
+template <bool BF16>
+__device__ __forceinline__ void mfma32_ordered(f32x16_t& acc, const u32x4& a, const u32x4& b) {
+    if constexpr (BF16)
+        asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b) : "memory");
+    else
+        asm volatile("v_mfma_f32_32x32x16_f16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b) : "memory");
+}
+
 template <bool BF16>
 __device__ __forceinline__ f32x4_t mfma16(u32x4 a, u32x4 b, f32x4_t c) {
     if constexpr (BF16)
@@ -526,6 +540,9 @@ void gas_kernel(const GasParams p) {
     using IO = TileIO<BM, BN, THREADS>;
     using acc_t = std::conditional_t<MF == 32, f32x16_t, f32x4_t>;
     constexpr int ACC_N = (MF == 32) ? 16 : 4;
+    // 256 x 256 tiles with 4 waves: one wave per SIMD holds a 128 x 128 block
+    // and the K loop stages 64 k at a time through registers (see below).
+    constexpr bool V4 = BM == 256 && BN == 256 && NW == 4 && MF == 32 && !CW && !RED;
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
 
@@ -684,6 +701,171 @@ void gas_kernel(const GasParams p) {
                 acc[i][j] = mfma16<BF16>(b, a, acc[i][j]);
         };
 
+        if constexpr (V4) {
+            // Four waves, one per SIMD, each a 128 x 128 block of 4 x 4 MFMA
+            // blocks.  A stage is 64 k: A as 256 rows of 128 bytes (whole cache
+            // lines, half the L2 requests of the ring loop's 64-byte rows), B
+            // as 64 rows of 512 bytes, both loaded into registers (no
+            // direct-to-LDS loads) and written to one of two LDS buffers by
+            // the waves during the stage before their reads, a whole stage
+            // after the load.  Within a stage the four k16 substeps are
+            // rotated like the ring loop: a substep's MFMAs use the fragments
+            // read in the substep before, and the last substep's MFMAs run
+            // after the next barrier.  With one wave per SIMD nothing else
+            // issues while the wave waits, so the MFMAs are ordered
+            // statements, one per slot, with the substep's fragment reads, LDS
+            // writes and loads placed in the slots between them.  Loads past
+            // the slice read zero (A through the offset bit, B past its
+            // resource), so every stage runs the same code.
+            constexpr int BK2 = 2 * BK;
+            constexpr int A2_BYTES = BM * BK2 * 2, B2_BYTES = BK2 * ROWB;
+            constexpr int BUF2 = A2_BYTES + B2_BYTES;
+            constexpr int LU = 8;                      // A (and B) loads per wave per stage
+            static_assert(2 * BUF2 <= LDS_BYTES && BM * BK2 * 2 == LU * NW * 1024 &&
+                          B2_BYTES == LU * NW * 1024 && MI == 4 && NI == 4 && ROWB == 512,
+                          "4-wave 256 x 256 staging");
+            const int S2 = (KT + 1) / 2;               // 64-k stages of the slice
+            const int kend2 = min(KT * BK, kend);      // k of the slice
+            const symtile::rsrc_t rA2 = symtile::make_rsrc(
+                p.A + (size_t)m0 * p.lda + kbeg, (uint32_t)(rows_a * p.lda * 2 - kbeg * 2));
+            const symtile::rsrc_t rB2 = symtile::make_rsrc(
+                p.B + (size_t)kbeg * p.ldb + n0,
+                kend2 > 0 ? (uint32_t)(((size_t)(kend2 - 1) * p.ldb + p.N - n0) * 2) : 0u);
+            // A: load u of wave w brings rows 32u + 8w + l/8, lane l chunk l%8;
+            // in LDS a row's chunk c sits at (c ^ ((row >> 1) & 7)), which for
+            // these rows is (4w + l/16) & 7 whatever u is.
+            const int a2g = lane & 7;
+            const uint32_t a2v = (uint32_t)((8 * wave + (lane >> 3)) * p.lda * 2 + a2g * 16);
+            const uint32_t a2u = (uint32_t)(32 * p.lda * 2);
+            // B: load u of wave w brings k-rows 8u + 2w + l/32, lane l chunk
+            // l%32, swizzled in LDS by bits 0, 1 and 3 of the row (bit 3 is
+            // u's parity).
+            const uint32_t b2v = (uint32_t)((2 * wave + (lane >> 5)) * p.ldb * 2 + (lane & 31) * 16);
+            const uint32_t b2u = (uint32_t)(8 * p.ldb * 2);
+            const uint32_t kb2 = (uint32_t)(BK2 * p.ldb * 2);
+
+            symtile::u32x4 P[2 * LU];                  // x < LU: A, else B
+            auto load_part = [&](int st, int u0, int u1) {
+                const int k0 = st * BK2;
+                const uint32_t va = a2v | ((uint32_t)(kend2 - 1 - k0 - 8 * a2g) & symtile::kOOB);
+#pragma unroll
+                for (int x = u0; x < u1; ++x) {
+                    if (x < LU)
+                        P[x] = symtile::buf_ld16p<symtile::kLoadDefault>(rA2, va, x * a2u + k0 * 2);
+                    else
+                        P[x] = symtile::buf_ld16p<symtile::kLoadDefault>(
+                            rB2, b2v, (x - LU) * b2u + (uint32_t)st * kb2);
+                }
+            };
+            // (The LDS addresses below are recomputed from `ln` in every stage:
+            // kept live across the loop they would not fit in registers.)
+            auto write_part = [&](int ln, int buf, int u0, int u1) {
+                uint8_t* As = smem + buf * BUF2;
+                uint8_t* Bs = As + A2_BYTES;
+                const uint32_t aw = (uint32_t)((8 * wave + (ln >> 3)) * (BK2 * 2) +
+                                               (((ln & 7) ^ ((4 * wave + (ln >> 4)) & 7)) << 4));
+                const int bk = 2 * wave + (ln >> 5), bc = ln & 31;
+#pragma unroll
+                for (int x = u0; x < u1; ++x) {
+                    if (x < LU) {
+                        *reinterpret_cast<symtile::u32x4*>(As + aw + x * 4096) = P[x];
+                    } else {
+                        const int u = x - LU;
+                        const uint32_t bw = (uint32_t)(bk * ROWB +
+                                                       ((bc ^ swz_b<CPR>(bk + 8 * (u & 1))) << 4));
+                        *reinterpret_cast<symtile::u32x4*>(Bs + bw + u * 4096) = P[x];
+                    }
+                }
+            };
+            symtile::u32x4 fa0[MI], fb0[NI], fa1[MI], fb1[NI];
+#pragma unroll
+            for (int i = 0; i < MI; ++i) fa1[i] = symtile::u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int j = 0; j < NI; ++j) fb1[j] = symtile::u32x4{0u, 0u, 0u, 0u};
+            // (wait states between the VALU writes above and the first MFMA)
+            asm volatile("s_nop 7\n\ts_nop 7" ::: "memory");
+            // One substep: its 16 MFMAs on the fragments read in the substep
+            // before (fa, fb), one per slot; the slots also carry this
+            // substep's 12 fragment reads (slots 0-5, into na, nb), a quarter
+            // of P to LDS (slots 6-9) and its reloads (slots 10-13), so that
+            // the wave issues something between any two MFMAs.
+            auto substep = [&](int ln, int buf, int t, int st,
+                               const symtile::u32x4 (&fa)[MI], const symtile::u32x4 (&fb)[NI],
+                               symtile::u32x4 (&na)[MI], symtile::u32x4 (&nb)[NI]) {
+                const uint8_t* As = smem + buf * BUF2;
+                const uint8_t* Bs = As + A2_BYTES;
+                const int c = 2 * t + (ln >> 5);
+                const int trr = 8 * (ln >> 5) + ((ln & 15) >> 2);
+                const int trc = 16 * ((ln >> 4) & 1) + 4 * (ln & 3);
+                u32x2_t h[NI][2];
+#pragma unroll
+                for (int q = 0; q < MI * NI; ++q) {
+                    mfma32_ordered<BF16>(acc[q / NI][q % NI], fb[q % NI], fa[q / NI]);
+                    if (q < 6) {
+                        // reads 2q and 2q+1 of a0..a3, b0 (two halves), .. b3
+#pragma unroll
+                        for (int r = 2 * q; r < 2 * q + 2; ++r) {
+                            if (r < MI) {
+                                const int row = wm * WM + r * MF + (ln & 31);
+                                na[r] = *reinterpret_cast<const symtile::u32x4*>(
+                                    As + row * (BK2 * 2) + ((c ^ ((row >> 1) & 7)) << 4));
+                            } else {
+                                const int j = (r - MI) / 2, half = (r - MI) % 2;
+                                const int col = wn * WN + j * MF + trc;
+                                const int k = 16 * t + trr + 4 * half;
+                                const uint8_t* qa = Bs + k * ROWB +
+                                                    (((col >> 3) ^ swz_b<CPR>(k)) << 4) +
+                                                    ((col & 4) << 1);
+                                h[j][half] = __builtin_bit_cast(
+                                    u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                 (__attribute__((address_space(3))) s16x4_t*)(qa)));
+                            }
+                        }
+                    } else if (q < 10) {
+                        write_part(ln, buf ^ 1, 4 * t + q - 6, 4 * t + q - 5);
+                    } else if (q < 14) {
+                        load_part(st + 2, 4 * t + q - 10, 4 * t + q - 9);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < NI; ++j)
+                    nb[j] = symtile::u32x4{h[j][0][0], h[j][0][1], h[j][1][0], h[j][1][1]};
+            };
+            // One stage: its fragments from buffer `buf`.  P holds stage st + 1
+            // (loaded during the stage before); in each substep a quarter of
+            // its registers goes to the other buffer (free since the barrier)
+            // and is reloaded at once with stage st + 2, so loads lead their
+            // LDS writes by a whole stage.
+            auto stage = [&](int st, int buf) {
+                int ln = lane;
+                asm volatile("" : "+v"(ln));
+                wait_lds<0>();
+                ring_barrier();
+                substep(ln, buf, 0, st, fa1, fb1, fa0, fb0);
+                substep(ln, buf, 1, st, fa0, fb0, fa1, fb1);
+                substep(ln, buf, 2, st, fa1, fb1, fa0, fb0);
+                substep(ln, buf, 3, st, fa0, fb0, fa1, fb1);
+            };
+            if (S2 > 0) {
+                load_part(0, 0, 2 * LU);
+                write_part(lane, 0, 0, 2 * LU);
+                load_part(1, 0, 2 * LU);
+                // (pairs of stages without a branch between them, so that the
+                // compiler's load waits stay exact across the loop's back edge)
+                int st = 0;
+                for (; st + 1 < S2; st += 2) {
+                    stage(st, 0);
+                    stage(st + 1, 1);
+                }
+                if (st < S2) stage(st, 0);
+                wait_lds<0>();
+#pragma unroll
+                for (int q = 0; q < MI * NI; ++q)     // last stage, substep 3
+                    mfma32_ordered<BF16>(acc[q / NI][q % NI], fb1[q % NI], fa1[q / NI]);
+            }
+            // (wait states between the last MFMA and reads of its result)
+            asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+        } else {
         // Pipeline over an LDS ring of NS stages of BK = 32, loads issued PD
         // stages ahead.  Each stage's fragment reads form two groups; the
         // loop is rotated so that the MFMAs of stage kt-1's second group
@@ -799,6 +981,7 @@ void gas_kernel(const GasParams p) {
             wait_lds<0>();
             mfmas1();              // last stage, group 1
         }
+        }  // V4
         __syncthreads();           // every wave is done with the ring
         if (p.trace && tid == 0 && ks == 0 && !reducer)
             tile_trace(p, tm, tn)[SYMTILE_TRACE_MAINLOOP] = symtile::clock_now();
@@ -1270,8 +1453,6 @@ Variant make_variant() {
 }
 
 // waves == 0 picks the first entry of the shape (the default wave count).
-// 256x256 tiles are built with 8 waves only: with 4 waves each wave holds a
-// 128x128 block (256 accumulator registers) and the compiler spills it.
 const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
     static const Variant table[] = {
         make_variant<64, 64, false, 4>(),    make_variant<64, 64, true, 4>(),
@@ -1280,6 +1461,7 @@ const Variant* find_variant(int bm, int bn, bool bf16, int waves) {
         make_variant<256, 128, false, 8, 32, true>(), make_variant<256, 128, true, 8, 32, true>(),
         make_variant<256, 128, false, 4>(),  make_variant<256, 128, true, 4>(),
         make_variant<256, 256, false, 8>(),  make_variant<256, 256, true, 8>(),
+        make_variant<256, 256, false, 4>(),  make_variant<256, 256, true, 4>(),
         make_variant<256, 224, false, 8, 16>(), make_variant<256, 224, true, 8, 16>(),
     };
     for (const Variant& v : table)

@@ -389,8 +389,8 @@ def test_argument_errors():
     with pytest.raises(pkg.SymtileError) as e:
         call(c0, f0, dtype=pkg.F32)
     assert e.value.name == "EUNSUPPORTED"
-    with pytest.raises(pkg.SymtileError) as e:           # 256x256 is built with 8 waves only
-        call(c0, f0, cfg=pkg.GasConfig(variant=FUSED, tile_m=256, tile_n=256, waves_per_wg=4))
+    with pytest.raises(pkg.SymtileError) as e:           # 256x224 is built with 8 waves only
+        call(c0, f0, cfg=pkg.GasConfig(variant=FUSED, tile_m=256, tile_n=224, waves_per_wg=4))
     assert e.value.name == "EUNSUPPORTED"
     p.heap.barrier()
 
@@ -493,6 +493,9 @@ def test_split_k_timeout_then_stale_workspace_is_reported(mode, again):
 
 
 @pytest.mark.parametrize("case", [(8, 1024, 1024, 4096, 256, 128, "bf16"),
+                                  (8, 1024, 1024, 4096, 256, 256, "bf16"),
+                                  (3, 300, 264, 200, 256, 256, "f16"),
+                                  (2, 520, 264, 72, 256, 256, "bf16"),
                                   (3, 300, 264, 200, 256, 128, "f16"),
                                   (2, 512, 256, 320, 256, 128, "bf16"),
                                   (4, 300, 264, 200, 128, 128, "bf16"),
@@ -511,6 +514,25 @@ def test_four_and_eight_wave_kernels_agree_bitwise(case):
         p.barrier()
         check_gathered(p, want, flag_count=int(p.calls[1 % world]))
         heaps.append(u16(p.out.C_all()).copy())
+    assert np.array_equal(heaps[0], heaps[1])
+
+
+@pytest.mark.parametrize("split", [2, 3])
+def test_four_wave_256_split_k_matches_eight_waves_bitwise(split):
+    """256 x 256 tiles with 4 waves stage 64 k at a time; K slices of an odd
+    number of 32-k stages end inside such a stage, whose k past the slice
+    must read zero.  The sums agree bit for bit with the 8-wave kernel's."""
+    world, M, N, K = 4, 512, 520, 4000 + 96
+    p = Problem(world, M, N, K, "bf16", 256, 256, seed=11)
+    want = {2: oracle_block(p.A, p.shards[2], "bf16")}
+    heaps = []
+    for waves in (4, 8):
+        p.sentinel()
+        p.run(2, FUSED, waves_per_wg=waves, split_k=split)
+        p.barrier()
+        check_gathered(p, want, flag_count=int(p.calls[2]))
+        heaps.append(u16(p.out.C_all()).copy())
+        assert np.all(_ws_counters(p) == 0)
     assert np.array_equal(heaps[0], heaps[1])
 
 
