@@ -86,6 +86,8 @@ def gas_profile_name(args, wl) -> str:
     sk = f"_k{args.split_k}" if args.split_k > 1 else ""
     if args.split_k > 1 and getattr(args, "split_reduce", 0):
         sk += f"_r{args.split_reduce}"
+    if getattr(args, "waves", 0):
+        sk += f"_w{args.waves}"
     if (args.variant, args.tile, args.nontemporal, args.gemm_wgs, args.copy_wgs,
             args.group_m, sk) == ("fused_seq", "256x256", 2, 0, 0, 0, ""):
         return f"gas_kernel_{wl.name}.md"
@@ -150,8 +152,8 @@ VARIANTS = ("bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec")
 
 # The configs array: (workload, schedule, tile, K slices, producer WGs,
 # consumer WGs, split-K reduction: 0 auto, 1 last slice, 2 banded, 3 reduction
-# kernel).  The headline leg (bf16 4096x8192.8192x3584, fused, 256x256) is not
-# repeated here.
+# kernel[, waves per producer workgroup]).  The headline leg (bf16
+# 4096x8192.8192x3584, fused, 256x256, 8 waves) is not repeated here.
 SWEEP = [
     ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0, 0),
     ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0, 0),
@@ -159,6 +161,7 @@ SWEEP = [
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 1),
     ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0, 0),
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0, 0),
+    ("gas_bf16_w8_m4096_k8192_n3584", "fused_seq", "256x256", 0, 0, 0, 0, 4),
     ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0, 0),
     ("gas_bf16_w8_m4096_k8192_n3584", "wave_spec", "256x128", 0, 0, 0, 0),
     ("gas_bf16_w8_m4096_k8192_n3584", "unfused_pc", "256x256", 0, 224, 32, 0),
@@ -243,7 +246,7 @@ def per_call_median_ms(launch, torch, n: int) -> float:
 
 
 def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps, warmup,
-            label_args, with_median=False, split_reduce=0, min_ms=0.0) -> dict:
+            label_args, with_median=False, split_reduce=0, min_ms=0.0, waves=None) -> dict:
     """One timed GEMM + All-Scatter configuration on `case`.  With min_ms > 0
     the number of timed launches is raised until they take about min_ms (from
     the settling phase's pace), so that the gap before the first launch of a
@@ -253,7 +256,7 @@ def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps,
          "unfused_pc": sym.UNFUSED_PC, "wave_spec": sym.WAVE_SPEC}[variant]
     kw = dict(gemm_wgs=gemm_wgs, copy_wgs=copy_wgs, nontemporal=args.nontemporal,
               group_m=args.group_m, split_k=split_k, split_reduce=split_reduce,
-              waves_per_wg=getattr(args, "waves", 0))
+              waves_per_wg=getattr(args, "waves", 0) if waves is None else waves)
 
     def launch():
         case.out.run(case.dA, case.dB, 0, v, **kw)
@@ -293,8 +296,10 @@ def gemm_bytes(wl) -> int:
 class _Label:
     """The argument names gas_profile_name reads, for a configs entry."""
 
-    def __init__(self, args, variant, tile, split_k, gemm_wgs, copy_wgs, split_reduce=0):
+    def __init__(self, args, variant, tile, split_k, gemm_wgs, copy_wgs, split_reduce=0,
+                 waves=0):
         self.variant, self.tile, self.split_k = variant, tile, split_k
+        self.waves = waves
         self.split_reduce = split_reduce
         self.gemm_wgs, self.copy_wgs = gemm_wgs, copy_wgs
         self.nontemporal, self.group_m = args.nontemporal, args.group_m
@@ -357,20 +362,22 @@ def bench_sweep(args, torch, sym, workload) -> list:
     built once."""
     out = []
     cases = {}
-    for name, variant, tile, split_k, g, c, red in SWEEP:
+    for entry in SWEEP:
+        name, variant, tile, split_k, g, c, red = entry[:7]
+        waves = entry[7] if len(entry) > 7 else 0
         key = (name, tile)
         if key not in cases:
             for k in list(cases):
                 cases.pop(k).close()
             cases[key] = GasCase(torch, sym, workload, workload.GEMM_WORKLOADS[name], tile)
         case = cases[key]
-        label = _Label(args, variant, tile, split_k, g, c, red)
+        label = _Label(args, variant, tile, split_k, g, c, red, waves)
         r = gas_leg(args, torch, sym, case, variant, split_k, g, c, args.sweep_steps, 5, label,
-                    split_reduce=red, min_ms=args.sweep_min_ms)
+                    split_reduce=red, min_ms=args.sweep_min_ms, waves=waves)
         wl = case.wl
         out.append({"workload": name, "dtype": wl.dtype, "schedule": variant, "tile": tile,
                     "split_k": max(split_k, 1), "split_reduce": red, "gemm_wgs": g,
-                    "copy_wgs": c,
+                    "copy_wgs": c, "waves": waves or None,
                     "ms": r["ms"], "value": r["tflops"], "unit": "TFLOP/s",
                     "steps": r["steps"], "settle": r["settle"],
                     "roofline": r["roofline"]})
