@@ -85,8 +85,10 @@ typedef struct {
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
                              (8 for 128x128 and the 256-row tiles, 4 for 64x64).
-                             Built: 64x64 with 4; 128x128 and 256x128 with 4 or 8;
-                             256x256 and 256x224 with 8 (others EUNSUPPORTED) */
+                             Built: 64x64 with 4; 128x128, 256x128 and 256x256
+                             with 4 or 8; 256x224 with 8 (others EUNSUPPORTED).
+                             256x256 with 4 stages 64 k at a time through
+                             registers; same results bit for bit */
     symtile_stream copy_stream; /* UNFUSED_PC: stream of the copy kernel; NULL = a
                              stream the heap creates on first use.  It must not
                              be the call's stream. */
