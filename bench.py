@@ -153,7 +153,8 @@ VARIANTS = ("bulk_sync", "fused_seq", "wg_spec", "unfused_pc", "wave_spec")
 # The configs array: (workload, schedule, tile, K slices, producer WGs,
 # consumer WGs, split-K reduction: 0 auto, 1 last slice, 2 banded, 3 reduction
 # kernel[, waves per producer workgroup]).  The headline leg (bf16
-# 4096x8192.8192x3584, fused, 256x256, 8 waves) is not repeated here.
+# 4096x8192.8192x3584, fused, 256x256, the default 4 waves) is not repeated
+# here; its 8-wave build is.
 SWEEP = [
     ("gas_f16_w2_m128_k256_n64", "fused_seq", "64x64", 0, 0, 0, 0),
     ("gas_f16_w2_m128_k256_n64", "wg_spec", "64x64", 0, 0, 0, 0),
@@ -161,7 +162,7 @@ SWEEP = [
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "128x128", 4, 0, 0, 1),
     ("gas_bf16_w8_m1024_k4096_n1024", "bulk_sync", "128x128", 4, 0, 0, 0),
     ("gas_bf16_w8_m1024_k4096_n1024", "fused_seq", "256x256", 16, 0, 0, 0),
-    ("gas_bf16_w8_m4096_k8192_n3584", "fused_seq", "256x256", 0, 0, 0, 0, 4),
+    ("gas_bf16_w8_m4096_k8192_n3584", "fused_seq", "256x256", 0, 0, 0, 0, 8),
     ("gas_bf16_w8_m4096_k8192_n3584", "bulk_sync", "256x256", 0, 0, 0, 0),
     ("gas_bf16_w8_m4096_k8192_n3584", "wave_spec", "256x128", 0, 0, 0, 0),
     ("gas_bf16_w8_m4096_k8192_n3584", "unfused_pc", "256x256", 0, 224, 32, 0),
@@ -281,10 +282,24 @@ def gas_leg(args, torch, sym, case, variant, split_k, gemm_wgs, copy_wgs, steps,
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": peak, "unit": "TFLOP/s",
                          "frac": tflops / peak, "traffic": traffic,
                          "traffic_profile": f"profiles/{prof}" if traffic is not None else None,
-                         "kernel": "gas_kernel<%d,%d,%s>" % (case.tm, case.tn, wl.dtype),
+                         "kernel": "gas_kernel<%d,%d,%s,%d waves>" % (
+                             case.tm, case.tn, wl.dtype,
+                             waves_used("%dx%d" % (case.tm, case.tn), variant, split_k,
+                                        kw["waves_per_wg"])),
                          "algorithmic_flops_per_launch": wl.flops,
                          "algorithmic_bytes_per_launch": gemm_bytes(wl),
                          "avg_launch_ms": ms}}
+
+
+def waves_used(tile: str, variant: str, split_k: int, waves: int) -> int:
+    """Waves per producer workgroup the library runs for these arguments
+    (waves 0 = the library's default for the tile and schedule)."""
+    if waves:
+        return waves
+    if tile == "64x64" or (tile == "256x256" and split_k <= 1 and
+                           variant in ("fused_seq", "bulk_sync")):
+        return 4
+    return 8
 
 
 def gemm_bytes(wl) -> int:

@@ -84,7 +84,8 @@ typedef struct {
                              line for the release to write back) */
     int group_m;          /* tile rows per L2 swizzle group; 0 = 4 */
     int waves_per_wg;     /* 4 or 8 wavefronts per workgroup; 0 = the tile's default
-                             (8 for 128x128 and the 256-row tiles, 4 for 64x64).
+                             (4 for 64x64, and for 256x256 in FUSED_SEQ and
+                             BULK_SYNC calls without split-K; 8 for the others).
                              Built: 64x64 with 4; 128x128, 256x128 and 256x256
                              with 4 or 8; 256x224 with 8 (others EUNSUPPORTED).
                              256x256 with 4 stages 64 k at a time through

@@ -1256,26 +1256,36 @@ void gas_kernel(const GasParams p) {
         // (banded split-K: only this slice's band is restaged and stored)
         // (the reduction kernel staged its band above)
         uint8_t* Cs = smem;
+        // (4-wave 256 x 256: the staging offsets are recomputed here from a
+        // lane value the compiler cannot hoist; computed before the K loop
+        // they were spilled and reloaded one at a time)
+        int lane_e = lane;
+        if constexpr (V4) asm volatile("" : "+v"(lane_e));
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
             if (RED || (banded && block_band(i) != ks)) continue;
 #pragma unroll
-            for (int j = 0; j < NI; ++j)
+            for (int j = 0; j < NI; ++j) {
+                // (4-wave 256 x 256: the block leaves its AGPRs only here, one
+                // block at a time; all at once they would not fit in VGPRs)
+                acc_t blk = acc[i][j];
+                if constexpr (V4) asm volatile("" : "+v"(blk));
 #pragma unroll
                 for (int g = 0; g < ACC_N / 4; ++g) {
                     // MF = 32: lane l, registers 4g..4g+3 hold row l % 32,
                     // columns 8g + 4 * (l / 32) .. +3 of the block; MF = 16:
                     // row l % 16, columns 4 * (l / 16) .. +3.
-                    const int row = wm * WM + i * MF + (lane % MF);
+                    const int row = wm * WM + i * MF + (lane_e % MF);
                     const int col = wn * WN + j * MF +
-                                    ((MF == 32) ? 8 * g + 4 * (lane >> 5) : 4 * (lane >> 4));
+                                    ((MF == 32) ? 8 * g + 4 * (lane_e >> 5) : 4 * (lane_e >> 4));
                     uint2 w;
-                    w.x = cvt_pack<BF16>(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
-                    w.y = cvt_pack<BF16>(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                    w.x = cvt_pack<BF16>(blk[4 * g + 0], blk[4 * g + 1]);
+                    w.y = cvt_pack<BF16>(blk[4 * g + 2], blk[4 * g + 3]);
                     const int chunk = col >> 3, half = (col >> 2) & 1;
                     *reinterpret_cast<uint2*>(Cs + row * CROW + ((chunk ^ (row & 7)) << 4) +
                                               (half << 3)) = w;
                 }
+            }
         }
         __syncthreads();
 
@@ -1607,7 +1617,16 @@ extern "C" symtile_status symtile_gemm_all_scatter(
     const int split = cfg.split_k > 1 ? cfg.split_k : 1;
     if (split > 1 && cfg.variant != SYMTILE_FUSED_SEQ && cfg.variant != SYMTILE_BULK_SYNC)
         return fail(SYMTILE_EUNSUPPORTED, "split_k > 1 is built for BULK_SYNC and FUSED_SEQ");
-    const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16, cfg.waves_per_wg);
+    // Default wave count: the shape's first build, except that unsplit
+    // 256 x 256 fused and bulk-synchronous calls run the 4-wave kernel (its
+    // register-staged loop is faster there; 8 waves stay for split-K, whose
+    // banded exchange favours them, and for the schedules with consumer
+    // workgroups, which take the producers' workgroup size).
+    int waves = cfg.waves_per_wg;
+    if (waves == 0 && cfg.tile_m == 256 && cfg.tile_n == 256 && split == 1 &&
+        (cfg.variant == SYMTILE_FUSED_SEQ || cfg.variant == SYMTILE_BULK_SYNC))
+        waves = 4;
+    const Variant* v = find_variant(cfg.tile_m, cfg.tile_n, dtype == SYMTILE_BF16, waves);
     if (!v) return fail(SYMTILE_EUNSUPPORTED, "tile shape / wave count not built");
     // Buffer resources span one tile row band of A or C and the whole of B;
     // each must stay below 2 GiB.
