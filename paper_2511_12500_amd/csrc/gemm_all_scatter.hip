@@ -787,7 +787,7 @@ void gas_kernel(const GasParams p) {
             // One substep: its 16 MFMAs on the fragments read in the substep
             // before (fa, fb), one per slot; the slots also carry this
             // substep's 12 fragment reads (slots 0-5, into na, nb), a quarter
-            // of P to LDS (slots 6-9) and its reloads (slots 10-13), so that
+            // of P to LDS and its reloads (alternating, slots 6-13), so that
             // the wave issues something between any two MFMAs.
             auto substep = [&](int ln, int buf, int t, int st,
                                const symtile::u32x4 (&fa)[MI], const symtile::u32x4 (&fb)[NI],
@@ -801,10 +801,18 @@ void gas_kernel(const GasParams p) {
 #pragma unroll
                 for (int q = 0; q < MI * NI; ++q) {
                     mfma32_ordered<BF16>(acc[q / NI][q % NI], fb[q % NI], fa[q / NI]);
-                    if (q < 6) {
-                        // reads 2q and 2q+1 of a0..a3, b0 (two halves), .. b3
+                    // slots 0-5: two fragment reads each; slots 6, 8, 10, 12:
+                    // the LDS writes, each followed in the next slot by the
+                    // reload of the same registers
+                    const int r0 = q < 6 ? 2 * q : 12, r1 = q < 6 ? 2 * q + 2 : 12;
+                    if (q >= 6 && q < 14 && !(q & 1))
+                        write_part(ln, buf ^ 1, 4 * t + (q - 6) / 2, 4 * t + (q - 6) / 2 + 1);
+                    if (q >= 7 && q < 14 && (q & 1))
+                        load_part(st + 2, 4 * t + (q - 7) / 2, 4 * t + (q - 7) / 2 + 1);
+                    if (r0 < r1) {
+                        // reads r0 .. r1-1 of a0..a3, b0 (two halves), .. b3
 #pragma unroll
-                        for (int r = 2 * q; r < 2 * q + 2; ++r) {
+                        for (int r = r0; r < r1; ++r) {
                             if (r < MI) {
                                 const int row = wm * WM + r * MF + (ln & 31);
                                 na[r] = *reinterpret_cast<const symtile::u32x4*>(
@@ -821,10 +829,6 @@ void gas_kernel(const GasParams p) {
                                                  (__attribute__((address_space(3))) s16x4_t*)(qa)));
                             }
                         }
-                    } else if (q < 10) {
-                        write_part(ln, buf ^ 1, 4 * t + q - 6, 4 * t + q - 5);
-                    } else if (q < 14) {
-                        load_part(st + 2, 4 * t + q - 10, 4 * t + q - 9);
                     }
                 }
 #pragma unroll
