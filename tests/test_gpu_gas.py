@@ -402,7 +402,8 @@ def test_padded_strides_on_tightly_sized_buffers():
     the result matches the oracle."""
     pkg = sym()
     world, rank, M, N, K, lda, ldb = 3, 1, 300, 136, 200, 264, 200
-    for tm, tn in ((128, 128), (256, 256), (64, 64)):
+    # (256 x 256 with both wave counts: 4 waves stage 64 k through registers)
+    for tm, tn, waves in ((128, 128, 0), (256, 256, 4), (256, 256, 8), (64, 64, 0)):
         p = Problem(world, M, N, K, "bf16", tm, tn, seed=21)
         bf = torch.bfloat16
         a_buf = torch.full(((M - 1) * lda + K,), float("nan"), dtype=bf, device="cuda")
@@ -414,7 +415,8 @@ def test_padded_strides_on_tightly_sized_buffers():
             pkg.symtile_gemm_all_scatter(
                 p.heap.handle, a_buf.data_ptr(), b_buf.data_ptr(), p.heap.ptr(rank, p.out.c_off),
                 p.heap.ptr(rank, p.out.flag_off), p.out.ready.data_ptr(), M, N, K, lda, ldb,
-                pkg.BF16, rank, world, pkg.GasConfig(variant=variant, tile_m=tm, tile_n=tn),
+                pkg.BF16, rank, world,
+                pkg.GasConfig(variant=variant, tile_m=tm, tile_n=tn, waves_per_wg=waves),
                 pkg.current_stream())
             p.calls[rank] += 1
             p.barrier()
